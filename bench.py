@@ -1,0 +1,242 @@
+"""Benchmark: trained words/sec of hierarchical-softmax skip-gram on one MI355X.
+
+One step = the whole path over the synthetic corpus, resident in HBM:
+vocabulary (count, order, remap), Huffman tree (codes, points), one training
+epoch (subsampling, window draws, path walks, top-31 LDS cache), held-out
+log-likelihood. value = in-vocabulary raw tokens of the epoch / step time
+(the classic tool's "words" count, taken before subsampling).
+
+The JSON line also carries the roofline of the training kernel (algorithmic
+bytes per launch from the byte model below, over the kernel's duration timed
+with HIP events on its stream) and the CPU oracle's rate on a bounded sample.
+
+Byte model, per kept centre v with P > 0 window words (fp32 rows of d floats):
+    8 d (len(v) - cached(v))   inner-node rows read and written once
+  + 8 d P                      window rows read once and updated once
+  + 4 len(v) + 9               path indices, code, length
+plus the cache traffic of each workgroup: fill 4 d k, write-back 8 d k per
+flush and at the end.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="sg_v1m_d300")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cache-k", type=int, default=31)
+    ap.add_argument("--flush-every", type=int, default=1000)
+    ap.add_argument("--flush-policy", type=int, default=1)
+    ap.add_argument("--write-policy", type=int, default=0)
+    ap.add_argument("--workers", type=int, default=0)
+    ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("train.hip", "w2v_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_1606_07822_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(torch, voc, tree, mask, doc_len, dim, k, flush_every, n_groups):
+    """Sum of the byte model over the epoch (see the module docstring)."""
+    V = voc.V
+    dev = mask.device
+    lens = tree.codelen.to(torch.int64)
+    first = V - 1 - k
+    seg = torch.repeat_interleave(torch.arange(V, device=dev), lens)
+    unc = torch.zeros(V, dtype=torch.int64, device=dev).index_add_(0, seg, (tree.points < first).to(torch.int64))
+    n = mask.numel()
+    n_docs = (n + doc_len - 1) // doc_len
+    m = torch.zeros(n_docs * doc_len, dtype=torch.bool, device=dev)
+    m[:n] = mask.bool()
+    per_doc = m.view(n_docs, doc_len).sum(1)
+    m.view(n_docs, doc_len)[per_doc < 2] = False          # centres without a window word do nothing
+    v = voc.tokens[m[:n]].to(torch.int64)
+    centres = int(v.numel())
+    node_rows = int(unc[v].sum().item())
+    path_len = int(lens[v].sum().item())
+    return centres, node_rows, path_len
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only; multi-GPU runs are not part of this build",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_1606_07822_amd as w2v
+    import synth
+
+    w = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    tok_np = synth.workload_corpus(w, threads=16)
+    held_np = synth.workload_corpus(w, heldout=True, threads=16)
+    log(f"generated {w.n_tokens:,} + {w.heldout_tokens:,} tokens in {time.time() - t0:.1f}s")
+    tok = torch.from_numpy(tok_np).to(dev)
+
+    # first pass builds the model's shapes (same vocabulary every step: deterministic)
+    voc = w2v.build_vocab(tok, w.vocab, w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    syn0, syn1 = synth.init_weights(voc.V, w.dim)
+    model = w2v.make_model(syn0, syn1, voc, tree, dev)
+    del syn0, syn1
+    p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, arch=w.arch, corpus_tokens=w.n_tokens,
+                   seed=synth.SEED_TRAIN, cache_k=args.cache_k, flush_every=args.flush_every,
+                   flush_policy=args.flush_policy, write_policy=args.write_policy, workers=args.workers)
+    pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
+    # held-out tokens as vocabulary indices (input preparation; the vocabulary is the same every step)
+    held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
+    ws = torch.empty(w2v.train_workspace_bytes(model, w.n_tokens, p), dtype=torch.uint8, device=dev)
+    stats = torch.zeros(w2v.N_STATS, dtype=torch.int64, device=dev)
+
+    # byte model of one launch (the sampler's keep mask with the training seed)
+    pr = w2v.sample_pairs(voc.tokens, voc.V, voc.vocab_counts, voc.train_words, p, cap=0, want_mask=True)
+    centres, node_rows, path_len = algorithmic_bytes(torch, voc, tree, pr.keep_mask, p.doc_len, w.dim,
+                                                     args.cache_k, args.flush_every, 0)
+    pairs = pr.total
+    del pr
+    torch.cuda.empty_cache()
+
+    def step():
+        v = w2v.build_vocab(tok, w.vocab, w.min_count)
+        t = w2v.build_huffman(v.vocab_counts)
+        model.tree = t
+        model.vocab_counts = v.vocab_counts
+        w2v.train_hs_epoch(model, v.tokens, p, stats=stats, workspace=ws)
+        kms = w2v.last_train_kernel_ms()
+        ll = None
+        if not args.no_loglik:
+            ll = w2v.hs_loglik(model, held, pe)
+        return kms, ll
+
+    for i in range(args.warmup):
+        step()
+        log(f"warmup {i} done")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    kms_all, lls = [], []
+    for i in range(args.steps):
+        kms, ll = step()
+        kms_all.append(kms)
+        lls.append(ll)
+        log(f"step {i} train kernel {kms:.1f} ms")
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    st = stats.cpu().numpy()
+    ms_per_step = dt * 1e3 / args.steps
+    words = int(st[1])
+    value = words / (ms_per_step / 1e3)
+    kernel_ms = sum(kms_all) / len(kms_all)
+
+    # roofline of the training kernel
+    d = w.dim
+    n_groups, n_waves = w2v.last_train_launch()
+    flushes = centres // max(1, args.flush_every) + n_groups
+    byte_total = (8 * d * node_rows + 8 * d * pairs + 4 * path_len + 9 * centres
+                  + n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k)
+    achieved = byte_total / (kernel_ms / 1e3) / 1e9
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+    if os.path.exists(tfile):
+        t = json.load(open(tfile))
+        if t.get("kernel_source") == kernel_source_hash():
+            traffic = t.get("hbm_bytes_per_launch")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, tok_np, args)
+
+    line = {
+        "metric": "trained words/sec, HS skip-gram V=1M d=300 fp32; % of HBM roofline",
+        "value": value,
+        "unit": "words/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Zipf + topic-mixture corpus standing in for the paper's text corpus)",
+        "config": {"workload": args.workload, "tokens": w.n_tokens, "vocab_ids": w.vocab, "V": voc.V, "dim": d,
+                   "window": w.window, "sample": w.sample, "min_count": w.min_count, "epochs_per_step": 1,
+                   "cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
+                   "write_policy": args.write_policy, "step": "vocab + huffman + epoch" +
+                   ("" if args.no_loglik else " + held-out loglik")},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic},
+        "train_kernel_ms": kernel_ms,
+        "train_kernel_words_per_s": words / (kernel_ms / 1e3),
+        "stats": dict(zip(w2v.STAT_NAMES, map(int, st))),
+        "pair_node_updates_per_s": int(st[4]) / (kernel_ms / 1e3),
+        "algorithmic_bytes_per_launch": byte_total,
+        "heldout_mean_ll": (lls[-1][0] / lls[-1][1]) if lls and lls[-1] else None,
+        "cpu_baseline": cpu,
+        "kernel_source": kernel_source_hash(),
+        "launch": {"workgroups": n_groups, "wavefronts": n_waves},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, tok_np, args):
+    """The oracle (single-threaded C) on a prefix of the same corpus, timed on this host."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    t0 = time.time()
+    voc = oracle.build_vocab(tok_np, w.vocab, w.min_count)
+    tree = oracle.build_huffman(voc.vocab_counts)
+    log(f"oracle vocabulary + tree in {time.time() - t0:.1f}s")
+    syn0, syn1 = synth.init_weights(voc.V, w.dim)
+    # calibrate on 2 documents, then size the sample to about cpu_seconds
+    n_cal = 2 * w.doc_len
+    tv = oracle.remap(tok_np[:n_cal], voc.id_to_vocab)
+    p = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, alpha0=w.alpha0, train_words=voc.train_words,
+                      corpus_tokens=w.n_tokens, seed=synth.SEED_TRAIN, cache_k=31, flush_every=10, arch=w.arch)
+    t0 = time.perf_counter()
+    oracle.train(syn0, syn1, tree, tv, p)
+    per_tok = (time.perf_counter() - t0) / n_cal
+    n = int(min(w.n_tokens, max(n_cal, args.cpu_seconds / max(per_tok, 1e-9))))
+    n = (n // w.doc_len) * w.doc_len or n_cal
+    syn0, syn1 = synth.init_weights(voc.V, w.dim)
+    tv = oracle.remap(tok_np[:n], voc.id_to_vocab)
+    t0 = time.perf_counter()
+    st = oracle.train(syn0, syn1, tree, tv, p)
+    dt = time.perf_counter() - t0
+    return {"value": float(st[1]) / dt, "unit": "words/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n:,} tokens ({n // w.doc_len} documents) of the same corpus, one epoch of "
+                      f"Algorithm 1 with the top-31 cache (u=10), {dt:.1f}s on one host core"}
+
+
+if __name__ == "__main__":
+    main()

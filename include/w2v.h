@@ -1,0 +1,224 @@
+/*
+ * w2v.h — C ABI of the MI355X (gfx950) hierarchical-softmax word2vec library.
+ *
+ * The library trains skip-gram (and CBOW) word vectors against a hierarchical
+ * softmax, as in Vuurens, Eickhoff and de Vries, "Efficient Parallel Learning
+ * of Word2Vec" (Algorithm 1, Cached Skipgram HS), including the paper's
+ * remedy for update collisions: the vectors of the top inner nodes of the
+ * Huffman tree are cached per worker and their change is written back
+ * periodically (§3.2). On the GPU the cache owner is a workgroup and the
+ * cache lives in LDS.
+ *
+ * Conventions (all entry points):
+ *   - Every pointer is a DEVICE pointer unless its name ends in _host.
+ *   - The caller owns all memory; the library never allocates device memory.
+ *     Scratch space comes in through (workspace, workspace_bytes); each call
+ *     has a *_workspace_bytes() query.
+ *   - Work is stream-ordered on hip_stream (a hipStream_t; NULL = the null
+ *     stream). Calls that write *_host outputs synchronise that stream before
+ *     returning; the others return without synchronising.
+ *   - Return value: W2V_OK or a negative w2v_status. Arguments are checked
+ *     before anything is launched; on W2V_E_ARG / W2V_E_RANGE /
+ *     W2V_E_WORKSPACE no output has been touched. On W2V_E_DEVICE outputs are
+ *     undefined. w2v_last_error() gives a message for the calling thread.
+ *   - Calls on different streams with disjoint buffers may run concurrently;
+ *     the only global state is the per-thread error message and a per-device
+ *     cache of device properties and timing events.
+ */
+#ifndef W2V_H
+#define W2V_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    W2V_OK = 0,
+    W2V_E_ARG = -1,        /* a null pointer, a size out of range, an inconsistent setting */
+    W2V_E_RANGE = -2,      /* data out of range: a token id outside [0, id_space), a code longer than 64 */
+    W2V_E_WORKSPACE = -3,  /* workspace_bytes below what the *_workspace_bytes query returns */
+    W2V_E_DEVICE = -4      /* a HIP runtime error (launch failure, fault surfaced at a synchronisation) */
+} w2v_status;
+
+/* Message for the calling thread's last non-OK return ("" if none). */
+const char *w2v_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Vocabulary (the "mintf" setting of §4.1; Algorithm 1 iterates over word
+ * ids of the text).
+ *
+ * Counts every id in tokens[0..n_tokens), keeps the ids whose count is at
+ * least min_count and orders them by (count descending, id ascending); the
+ * position in that order is the vocabulary index 0..V-1.
+ *   tokens        int32[n_tokens], ids in [0, id_space)
+ *   counts_by_id  int64[id_space]  out: occurrences of each id
+ *   vocab_ids     int32[id_space]  out: id of vocabulary index r (r < V); -1 beyond V
+ *   vocab_counts  int64[id_space]  out: count of vocabulary index r (r < V); 0 beyond V
+ *   id_to_vocab   int32[id_space]  out: vocabulary index of each id, -1 if dropped
+ *   tokens_out    int32[n_tokens]  out, may be NULL: tokens mapped to vocabulary
+ *                                  indices (-1 = dropped); may not alias tokens
+ *   V_host, train_words_host       out: V and the sum of kept counts
+ * Errors: W2V_E_RANGE if a token lies outside [0, id_space) (outputs are then
+ * written but invalid); W2V_E_ARG if id_space < 1, n_tokens < 0 or
+ * min_count < 0. Synchronises the stream.
+ * ---------------------------------------------------------------------- */
+size_t w2v_build_vocab_workspace_bytes(int32_t id_space);
+int w2v_build_vocab(const int32_t *tokens, int64_t n_tokens, int32_t id_space, int64_t min_count,
+                    int64_t *counts_by_id, int32_t *vocab_ids, int64_t *vocab_counts, int32_t *id_to_vocab,
+                    int32_t *tokens_out, int32_t *V_host, int64_t *train_words_host, void *workspace,
+                    size_t workspace_bytes, void *hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Huffman tree (§2: the output layer is a binary Huffman tree; a word is
+ * predicted by the turns at the inner nodes on its path from the root).
+ *
+ * Built from vocab_counts[0..V) (descending) by the two-queue merge: leaves in
+ * ascending count (vocabulary index V-1 first), inner nodes in creation order;
+ * each merge takes the smaller front twice, a leaf winning a count tie; the
+ * first child taken gets bit 0; merge a creates inner node a; the root is V-2.
+ *   codelen    uint8[V]     out: depth of each word
+ *   code       uint64[V]    out: bit j = turn at the j-th inner node from the root
+ *   point_off  int32[V+1]   out: word v's inner nodes are points[point_off[v] ..
+ *                           point_off[v+1]), root first
+ *   points     int32[points_cap] out; NULL = size query (only codelen, code,
+ *                           point_off and the host outputs are written)
+ *   points_len_host, max_len_host  out: sum of code lengths, longest code
+ * Errors: W2V_E_ARG if V < 2 or points_cap < sum of lengths (points given);
+ * W2V_E_RANGE if a code would be longer than 64. Synchronises the stream.
+ * ---------------------------------------------------------------------- */
+size_t w2v_build_huffman_workspace_bytes(int32_t V);
+int w2v_build_huffman(const int64_t *vocab_counts, int32_t V, uint8_t *codelen, uint64_t *code,
+                      int32_t *point_off, int32_t *points, int64_t points_cap, int64_t *points_len_host,
+                      int32_t *max_len_host, void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Model and training settings.
+ *
+ * syn0 ("vector[w]" of Algorithm 1) is float[V][row_stride], syn1
+ * ("weight[n]", the inner-node vectors) is float[V-1][row_stride]; only the
+ * first dim floats of a row are used. row_stride >= dim, a multiple of 4;
+ * both arrays 16-byte aligned.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    float *syn0;
+    float *syn1;
+    int32_t V, dim, row_stride;
+    int32_t reserved0;
+    const int64_t *vocab_counts;  /* int64[V] from w2v_build_vocab (keep probabilities) */
+    int64_t train_words;          /* sum of vocab_counts (N_t) */
+    const uint8_t *codelen;       /* from w2v_build_huffman */
+    const uint64_t *code;
+    const int32_t *point_off;
+    const int32_t *points;
+} w2v_model;
+
+typedef struct {
+    int32_t arch;            /* 0 = skip-gram (Algorithm 1), 1 = CBOW (mean of the window as input) */
+    int32_t mode;            /* 0 = asynchronous (lock-free, top-k cache in LDS), 1 = synchronous batches */
+    int32_t window;          /* W ("windowsize", §4.1), 1..10; effective half-width uniform on 1..W */
+    int32_t doc_len;         /* documents of doc_len raw tokens (1..65535); windows never cross them */
+    double sample;           /* subsampling threshold t ("downsample", §4.1); 0 = keep all */
+    float alpha0;            /* initial learning rate */
+    int32_t epoch, n_epochs; /* this epoch and the total, for the learning-rate schedule */
+    int32_t reserved1;
+    int64_t corpus_tokens;   /* raw tokens of one epoch (the whole corpus, for the schedule) */
+    int64_t first_raw_index; /* global raw index of tokens[0]; a multiple of doc_len */
+    uint64_t seed;           /* Philox4x32-10 key for subsampling and window draws */
+    int32_t cache_k;         /* inner nodes cached per workgroup ("isFrequent"): the k created last */
+    int32_t flush_every;     /* write the cache back after this many centre words per workgroup (>= 1) */
+    int32_t sync_batch;      /* synchronous mode: kept centres per batch (>= 1) */
+    int32_t workers;         /* wavefronts that take documents; 0 = fill the GPU; 1 = one sequential worker */
+    int32_t write_policy;    /* uncached inner nodes: 0 = atomic add of the change, 1 = plain store */
+    int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), 1 = add the
+                                change divided by the number of workgroups (their progress averaged) */
+    int32_t reserved2[6];
+} w2v_params;
+
+/* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,
+   node updates (pair-node updates for skip-gram, centre-node updates for CBOW). */
+#define W2V_N_STATS 5
+
+/* ------------------------------------------------------------------------
+ * One training pass over tokens[0..n_tokens) (vocabulary indices, -1 =
+ * dropped), updating m->syn0 and m->syn1 in place.
+ *
+ * Per kept centre word v (subsampling: keep with probability
+ * min(1, sqrt(q) + q), q = t N_t / count(v), drawn from Philox4x32-10 keyed
+ * by (seed; raw index, epoch)), with window words w_1..w_P (the kept words of
+ * the same document within the effective half-width), the path of v is
+ * walked once; at each inner node n with turn t and every window word in
+ * order: f = sigmoid(syn0[w].syn1[n]), g = (1 - t - f) alpha, the
+ * hidden-layer gradient of w gains g syn1[n] and syn1[n] gains g syn0[w];
+ * afterwards each syn0[w] gains its hidden-layer gradient (Algorithm 1 with
+ * the window and node loops swapped, which is the same computation whenever
+ * a window holds no repeated word). alpha decays linearly with the raw stream
+ * position in steps of 10,000 tokens down to 1e-4 alpha0.
+ *
+ * mode 0: documents are claimed by wavefronts from a queue; the top cache_k
+ * inner-node vectors live in each workgroup's LDS and are written back as a
+ * change (cached - original) every flush_every centres (§3.2); other rows are
+ * updated in HBM with atomic adds of their change. Lock-free: results vary
+ * with scheduling, as in the paper's Hogwild setting, except with workers=1.
+ * mode 1: every gradient of a batch of sync_batch consecutive kept centres
+ * uses the model at the start of the batch; the sums (exact int64 fixed
+ * point) are applied at its end. Deterministic. Synchronises the stream once
+ * (to read the number of kept centres).
+ * stats: int64[W2V_N_STATS] device buffer, overwritten (may be NULL).
+ * Errors: W2V_E_ARG for a bad model/params (V < 2, dim not in 1..1024,
+ * window not in 1..10, LDS budget 2 cache_k dim 4 bytes exceeded, ...).
+ * ---------------------------------------------------------------------- */
+size_t w2v_train_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
+int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,
+                       int64_t *stats, void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/* Duration in milliseconds of the main training kernel of the last
+   w2v_train_hs_epoch call on the calling thread's current device (HIP events
+   recorded on that call's stream). Waits for that kernel to finish. */
+int w2v_last_train_kernel_ms(float *ms_host);
+
+/* Launch shape of the main training kernel of the last asynchronous
+   w2v_train_hs_epoch call on the calling thread's current device: workgroups
+   (cache owners) and wavefronts that took documents. Host-side, no wait. */
+int w2v_last_train_launch(int32_t *workgroups_host, int32_t *wavefronts_host);
+
+/* ------------------------------------------------------------------------
+ * Hierarchical-softmax log-likelihood (evaluation): over the (centre,
+ * context) pairs that the sampler draws from tokens with p's seed, epoch,
+ * window and sample settings, sum_ll = sum of log P(v | syn0[w]) with
+ * P(v|x) = prod_j sigmoid((1 - 2 t_j) x . syn1[n_j]) over v's path.
+ * Dot products in fp32, logarithms and sums in fp64, summed in a fixed order
+ * (deterministic). Read-only on the model. Synchronises the stream.
+ * ---------------------------------------------------------------------- */
+size_t w2v_hs_loglik_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
+int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,
+                  double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, void *workspace,
+                  size_t workspace_bytes, void *hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Test hooks (not part of the training contract).
+ *
+ * w2v_sample_pairs: the (centre, context) pairs of the sampler in stream
+ * order (documents, then centres, then window positions ascending), as global
+ * raw indices; the first pair_cap are written (centre_raw/context_raw may be
+ * NULL); keep_mask uint8[n_tokens] (may be NULL) marks kept centres;
+ * checksum_host = sum over all pairs of fmix64(centre * 0x9E3779B97F4A7C15 +
+ * context) mod 2^64 (MurmurHash3 finaliser). Synchronises the stream.
+ *
+ * w2v_keep_thresholds: thr[v] = 2^32 if the keep probability is >= 1, else
+ * floor(p_keep 2^32); a token is kept iff its first Philox word < thr.
+ * ---------------------------------------------------------------------- */
+size_t w2v_sample_pairs_workspace_bytes(int32_t V, int64_t n_tokens, const w2v_params *p);
+int w2v_sample_pairs(const int32_t *tokens, int64_t n_tokens, int32_t V, const int64_t *vocab_counts,
+                     int64_t train_words, const w2v_params *p, int64_t *centre_raw, int64_t *context_raw,
+                     int64_t pair_cap, uint8_t *keep_mask, int64_t *n_pairs_host, int64_t *n_kept_host,
+                     uint64_t *checksum_host, void *workspace, size_t workspace_bytes, void *hip_stream);
+int w2v_keep_thresholds(const int64_t *vocab_counts, int32_t V, double sample, int64_t train_words, uint64_t *thr,
+                        void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* W2V_H */

@@ -1,0 +1,359 @@
+"""MI355X hierarchical-softmax word2vec: Python binding of libw2v.so.
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+PyTorch provides device memory and the current stream. The library never
+allocates device memory; workspaces are torch uint8 tensors made here.
+
+Entry points mirror the C ABI in include/w2v.h:
+    build_vocab, build_huffman, train_hs_epoch, hs_loglik
+plus the test hooks sample_pairs and keep_thresholds.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libw2v.so")
+
+W2V_OK, W2V_E_ARG, W2V_E_RANGE, W2V_E_WORKSPACE, W2V_E_DEVICE = 0, -1, -2, -3, -4
+N_STATS = 5
+STAT_NAMES = ("raw_tokens", "in_vocab_tokens", "kept_centres", "pairs", "node_updates")
+
+P = ctypes.c_void_p
+I32, I64, U64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+
+
+class W2VError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"w2v error {code}: {msg}")
+        self.code = code
+
+
+class CModel(ctypes.Structure):
+    _fields_ = [("syn0", P), ("syn1", P), ("V", I32), ("dim", I32), ("row_stride", I32), ("reserved0", I32),
+                ("vocab_counts", P), ("train_words", I64), ("codelen", P), ("code", P), ("point_off", P),
+                ("points", P)]
+
+
+class CParams(ctypes.Structure):
+    _fields_ = [("arch", I32), ("mode", I32), ("window", I32), ("doc_len", I32), ("sample", ctypes.c_double),
+                ("alpha0", ctypes.c_float), ("epoch", I32), ("n_epochs", I32), ("reserved1", I32),
+                ("corpus_tokens", I64), ("first_raw_index", I64), ("seed", U64), ("cache_k", I32),
+                ("flush_every", I32), ("sync_batch", I32), ("workers", I32), ("write_policy", I32),
+                ("flush_policy", I32), ("reserved2", I32 * 6)]
+
+
+assert ctypes.sizeof(CModel) == 80 and ctypes.sizeof(CParams) == 112
+
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libw2v.so; raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(there is no fallback implementation)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.w2v_last_error.restype = ctypes.c_char_p
+        L.w2v_last_error.argtypes = []
+        L.w2v_build_vocab_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_build_vocab_workspace_bytes.argtypes = [I32]
+        L.w2v_build_vocab.restype = ctypes.c_int
+        L.w2v_build_vocab.argtypes = [P, I64, I32, I64, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+        L.w2v_build_huffman_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_build_huffman_workspace_bytes.argtypes = [I32]
+        L.w2v_build_huffman.restype = ctypes.c_int
+        L.w2v_build_huffman.argtypes = [P, I32, P, P, P, P, I64, P, P, P, ctypes.c_size_t, P]
+        L.w2v_train_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_train_workspace_bytes.argtypes = [ctypes.POINTER(CModel), I64, ctypes.POINTER(CParams)]
+        L.w2v_train_hs_epoch.restype = ctypes.c_int
+        L.w2v_train_hs_epoch.argtypes = [ctypes.POINTER(CModel), P, I64, ctypes.POINTER(CParams), P, P,
+                                         ctypes.c_size_t, P]
+        L.w2v_last_train_kernel_ms.restype = ctypes.c_int
+        L.w2v_last_train_kernel_ms.argtypes = [ctypes.POINTER(ctypes.c_float)]
+        L.w2v_last_train_launch.restype = ctypes.c_int
+        L.w2v_last_train_launch.argtypes = [ctypes.POINTER(I32), ctypes.POINTER(I32)]
+        L.w2v_hs_loglik_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_hs_loglik_workspace_bytes.argtypes = [ctypes.POINTER(CModel), I64, ctypes.POINTER(CParams)]
+        L.w2v_hs_loglik.restype = ctypes.c_int
+        L.w2v_hs_loglik.argtypes = [ctypes.POINTER(CModel), P, I64, ctypes.POINTER(CParams), P, P, P, P,
+                                    ctypes.c_size_t, P]
+        L.w2v_sample_pairs_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_sample_pairs_workspace_bytes.argtypes = [I32, I64, ctypes.POINTER(CParams)]
+        L.w2v_sample_pairs.restype = ctypes.c_int
+        L.w2v_sample_pairs.argtypes = [P, I64, I32, P, I64, ctypes.POINTER(CParams), P, P, I64, P, P, P, P, P,
+                                       ctypes.c_size_t, P]
+        L.w2v_keep_thresholds.restype = ctypes.c_int
+        L.w2v_keep_thresholds.argtypes = [P, I32, ctypes.c_double, I64, P, P]
+        _LIB = L
+    return _LIB
+
+
+def last_error() -> str:
+    return lib().w2v_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != W2V_OK:
+        raise W2VError(rc, last_error())
+
+
+def _dev_ptr(t: torch.Tensor | None, dtype: torch.dtype, name: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(device: torch.device | None = None) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------- vocabulary
+@dataclass
+class Vocab:
+    counts_by_id: torch.Tensor   # int64[id_space]
+    vocab_ids: torch.Tensor      # int32[V]
+    vocab_counts: torch.Tensor   # int64[V]
+    id_to_vocab: torch.Tensor    # int32[id_space]
+    V: int
+    train_words: int
+    tokens: torch.Tensor | None  # int32[n] vocabulary indices (-1 = dropped)
+
+
+def build_vocab(tokens: torch.Tensor, id_space: int, min_count: int = 5, remap: bool = True) -> Vocab:
+    """Count ids, keep count >= min_count, order by (count desc, id asc); optionally remap tokens."""
+    dev = tokens.device
+    n = tokens.numel()
+    counts = torch.empty(id_space, dtype=torch.int64, device=dev)
+    ids = torch.empty(id_space, dtype=torch.int32, device=dev)
+    vc = torch.empty(id_space, dtype=torch.int64, device=dev)
+    i2v = torch.empty(id_space, dtype=torch.int32, device=dev)
+    out = torch.empty(n, dtype=torch.int32, device=dev) if remap else None
+    ws = _workspace(lib().w2v_build_vocab_workspace_bytes(id_space), dev)
+    V = ctypes.c_int32(0)
+    tw = ctypes.c_int64(0)
+    _check(lib().w2v_build_vocab(_dev_ptr(tokens, torch.int32, "tokens"), n, id_space, min_count,
+                                 counts.data_ptr(), ids.data_ptr(), vc.data_ptr(), i2v.data_ptr(),
+                                 out.data_ptr() if out is not None else None, ctypes.byref(V), ctypes.byref(tw),
+                                 ws.data_ptr(), ws.numel(), _stream(dev)))
+    v = V.value
+    return Vocab(counts, ids[:v], vc[:v], i2v, v, tw.value, out)
+
+
+# ---------------------------------------------------------------- Huffman
+@dataclass
+class Tree:
+    codelen: torch.Tensor    # uint8[V]
+    code: torch.Tensor       # int64[V] (bit patterns of uint64)
+    point_off: torch.Tensor  # int32[V+1]
+    points: torch.Tensor     # int32[sum len]
+    max_len: int
+
+
+def build_huffman(vocab_counts: torch.Tensor) -> Tree:
+    dev = vocab_counts.device
+    V = vocab_counts.numel()
+    vc = vocab_counts.contiguous()
+    codelen = torch.empty(V, dtype=torch.uint8, device=dev)
+    code = torch.empty(V, dtype=torch.int64, device=dev)
+    off = torch.empty(V + 1, dtype=torch.int32, device=dev)
+    ws = _workspace(lib().w2v_build_huffman_workspace_bytes(V), dev)
+    plen = ctypes.c_int64(0)
+    mlen = ctypes.c_int32(0)
+    # one call with a points buffer of the largest possible size would waste memory; size first
+    _check(lib().w2v_build_huffman(_dev_ptr(vc, torch.int64, "vocab_counts"), V, codelen.data_ptr(),
+                                   code.data_ptr(), off.data_ptr(), None, 0, ctypes.byref(plen), ctypes.byref(mlen),
+                                   ws.data_ptr(), ws.numel(), _stream(dev)))
+    points = torch.empty(max(plen.value, 1), dtype=torch.int32, device=dev)
+    _check(lib().w2v_build_huffman(vc.data_ptr(), V, codelen.data_ptr(), code.data_ptr(), off.data_ptr(),
+                                   points.data_ptr(), points.numel(), ctypes.byref(plen), ctypes.byref(mlen),
+                                   ws.data_ptr(), ws.numel(), _stream(dev)))
+    return Tree(codelen, code, off, points[:plen.value], mlen.value)
+
+
+# ---------------------------------------------------------------- model
+def padded_stride(dim: int) -> int:
+    """Row stride in floats: dim rounded up to 32 (128-byte rows)."""
+    return (dim + 31) // 32 * 32
+
+
+@dataclass
+class Model:
+    syn0: torch.Tensor          # float32[V, stride]
+    syn1: torch.Tensor          # float32[V-1, stride]
+    dim: int
+    vocab_counts: torch.Tensor  # int64[V]
+    train_words: int
+    tree: Tree
+
+    @property
+    def V(self) -> int:
+        return self.syn0.shape[0]
+
+    @property
+    def stride(self) -> int:
+        return self.syn0.shape[1]
+
+    def c(self) -> CModel:
+        for name, t in (("syn0", self.syn0), ("syn1", self.syn1)):
+            _dev_ptr(t, torch.float32, name)
+        return CModel(self.syn0.data_ptr(), self.syn1.data_ptr(), self.V, self.dim, self.stride, 0,
+                      _dev_ptr(self.vocab_counts, torch.int64, "vocab_counts"), self.train_words,
+                      self.tree.codelen.data_ptr(), self.tree.code.data_ptr(), self.tree.point_off.data_ptr(),
+                      self.tree.points.data_ptr())
+
+    def vectors(self) -> tuple[torch.Tensor, torch.Tensor]:
+        """(syn0[:, :dim], syn1[:, :dim]) views."""
+        return self.syn0[:, :self.dim], self.syn1[:, :self.dim]
+
+
+def make_model(syn0_init, syn1_init, vocab: Vocab, tree: Tree, device="cuda") -> Model:
+    """Copy [V, dim] initial weights (numpy or torch) into padded device rows."""
+    s0 = torch.as_tensor(syn0_init, dtype=torch.float32)
+    s1 = torch.as_tensor(syn1_init, dtype=torch.float32)
+    V, dim = s0.shape
+    stride = padded_stride(dim)
+    syn0 = torch.zeros(V, stride, dtype=torch.float32, device=device)
+    syn1 = torch.zeros(max(V - 1, 1), stride, dtype=torch.float32, device=device)
+    syn0[:, :dim].copy_(s0)
+    syn1[:V - 1, :dim].copy_(s1)
+    return Model(syn0, syn1, dim, vocab.vocab_counts.contiguous(), vocab.train_words, tree)
+
+
+@dataclass
+class Params:
+    window: int
+    sample: float = 0.0
+    alpha0: float = 0.025
+    arch: int = 0
+    mode: int = 0
+    doc_len: int = 1000
+    epoch: int = 0
+    n_epochs: int = 1
+    corpus_tokens: int = 0
+    first_raw_index: int = 0
+    seed: int = 3
+    cache_k: int = 31
+    flush_every: int = 1000
+    sync_batch: int = 4096
+    workers: int = 0
+    write_policy: int = 0
+    flush_policy: int = 1
+    extra: dict = field(default_factory=dict)
+
+    def c(self) -> CParams:
+        return CParams(self.arch, self.mode, self.window, self.doc_len, float(self.sample), float(self.alpha0),
+                       self.epoch, self.n_epochs, 0, self.corpus_tokens, self.first_raw_index, self.seed,
+                       self.cache_k, self.flush_every, self.sync_batch, self.workers, self.write_policy,
+                       self.flush_policy)
+
+
+# ---------------------------------------------------------------- training
+def train_hs_epoch(model: Model, tokens: torch.Tensor, p: Params, stats: torch.Tensor | None = None,
+                   workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """One pass over tokens (vocabulary indices). Returns the device stats tensor int64[5]; does not sync."""
+    dev = tokens.device
+    cm, cp = model.c(), p.c()
+    if cp.corpus_tokens <= 0:
+        cp.corpus_tokens = tokens.numel()
+    need = lib().w2v_train_workspace_bytes(ctypes.byref(cm), tokens.numel(), ctypes.byref(cp))
+    if workspace is None or workspace.numel() < need:
+        workspace = _workspace(need, dev)
+    if stats is None:
+        stats = torch.zeros(N_STATS, dtype=torch.int64, device=dev)
+    _check(lib().w2v_train_hs_epoch(ctypes.byref(cm), _dev_ptr(tokens, torch.int32, "tokens"), tokens.numel(),
+                                    ctypes.byref(cp), _dev_ptr(stats, torch.int64, "stats"), workspace.data_ptr(),
+                                    workspace.numel(), _stream(dev)))
+    return stats
+
+
+def train_workspace_bytes(model: Model, n_tokens: int, p: Params) -> int:
+    cm, cp = model.c(), p.c()
+    if cp.corpus_tokens <= 0:
+        cp.corpus_tokens = n_tokens
+    return int(lib().w2v_train_workspace_bytes(ctypes.byref(cm), n_tokens, ctypes.byref(cp)))
+
+
+def last_train_kernel_ms() -> float:
+    ms = ctypes.c_float(0)
+    _check(lib().w2v_last_train_kernel_ms(ctypes.byref(ms)))
+    return float(ms.value)
+
+
+def last_train_launch() -> tuple[int, int]:
+    """(workgroups, wavefronts) of the last asynchronous training launch."""
+    g = ctypes.c_int32(0)
+    wv = ctypes.c_int32(0)
+    _check(lib().w2v_last_train_launch(ctypes.byref(g), ctypes.byref(wv)))
+    return g.value, wv.value
+
+
+def hs_loglik(model: Model, tokens: torch.Tensor, p: Params):
+    """(sum of log P(v|w) over the sampler's pairs, n_pairs, n_nodes). Synchronises."""
+    dev = tokens.device
+    cm, cp = model.c(), p.c()
+    ws = _workspace(lib().w2v_hs_loglik_workspace_bytes(ctypes.byref(cm), tokens.numel(), ctypes.byref(cp)), dev)
+    s = ctypes.c_double(0)
+    npairs = ctypes.c_int64(0)
+    nn = ctypes.c_int64(0)
+    _check(lib().w2v_hs_loglik(ctypes.byref(cm), _dev_ptr(tokens, torch.int32, "tokens"), tokens.numel(),
+                               ctypes.byref(cp), ctypes.byref(s), ctypes.byref(npairs), ctypes.byref(nn),
+                               ws.data_ptr(), ws.numel(), _stream(dev)))
+    return s.value, npairs.value, nn.value
+
+
+# ---------------------------------------------------------------- test hooks
+@dataclass
+class Pairs:
+    centre: torch.Tensor | None
+    context: torch.Tensor | None
+    total: int
+    n_kept: int
+    checksum: int
+    keep_mask: torch.Tensor | None
+
+
+def sample_pairs(tokens: torch.Tensor, V: int, vocab_counts: torch.Tensor, train_words: int, p: Params,
+                 cap: int = 0, want_mask: bool = False) -> Pairs:
+    dev = tokens.device
+    cp = p.c()
+    n = tokens.numel()
+    ws = _workspace(lib().w2v_sample_pairs_workspace_bytes(V, n, ctypes.byref(cp)), dev)
+    c = torch.empty(max(cap, 1), dtype=torch.int64, device=dev)
+    x = torch.empty(max(cap, 1), dtype=torch.int64, device=dev)
+    mask = torch.empty(max(n, 1), dtype=torch.uint8, device=dev) if want_mask else None
+    npairs = ctypes.c_int64(0)
+    nk = ctypes.c_int64(0)
+    cs = ctypes.c_uint64(0)
+    _check(lib().w2v_sample_pairs(_dev_ptr(tokens, torch.int32, "tokens"), n, V,
+                                  _dev_ptr(vocab_counts, torch.int64, "vocab_counts"), train_words, ctypes.byref(cp),
+                                  c.data_ptr() if cap else None, x.data_ptr() if cap else None, cap,
+                                  mask.data_ptr() if mask is not None else None, ctypes.byref(npairs),
+                                  ctypes.byref(nk), ctypes.byref(cs), ws.data_ptr(), ws.numel(), _stream(dev)))
+    m = min(cap, npairs.value)
+    return Pairs(c[:m] if cap else None, x[:m] if cap else None, npairs.value, nk.value, cs.value,
+                 mask[:n] if mask is not None else None)
+
+
+def keep_thresholds(vocab_counts: torch.Tensor, sample: float, train_words: int) -> torch.Tensor:
+    V = vocab_counts.numel()
+    thr = torch.empty(V, dtype=torch.int64, device=vocab_counts.device)
+    _check(lib().w2v_keep_thresholds(_dev_ptr(vocab_counts, torch.int64, "vocab_counts"), V, float(sample),
+                                     train_words, thr.data_ptr(), _stream(vocab_counts.device)))
+    return thr

@@ -1,0 +1,443 @@
+// Deterministic synchronous training mode and the HS log-likelihood evaluator.
+//
+// Synchronous mode: every gradient of a batch of B consecutive kept centres is
+// taken against the model as it stood at the start of the batch; the changes
+// are summed exactly as int64 fixed point (value * 2^kFrac, integer atomics
+// commute, so the sums do not depend on scheduling) and applied after the
+// batch: row = row + (float)(sum * 2^-kFrac).
+//
+// Log-likelihood: sum over the sampler's pairs (v, w) of
+// log P(v | syn0[w]) = sum_j log sigmoid((1 - 2 t_j) syn0[w] . syn1[n_j]);
+// dot products in fp32, logarithms and all sums in fp64, in a fixed order.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "w2v_internal.h"
+
+namespace w2v {
+
+constexpr int kFrac = 40;   // fixed-point fraction bits of the synchronous-mode sums
+
+struct SyncArgs {
+    const float *syn0;
+    const float *syn1;
+    int32_t V, dim, stride;
+    const uint8_t *codelen;
+    const uint64_t *code;
+    const int32_t *point_off;
+    const int32_t *points;
+    const int32_t *kept_vid;
+    const uint32_t *kept_meta;
+    const int32_t *doc_kept;
+    const int64_t *kept_off;   // exclusive prefix of doc_kept
+    int64_t n_docs;
+    int32_t doc_len;
+    int64_t first_raw, epoch_base;
+    const float *alpha_tab;
+    int64_t blk0;
+    int64_t c_lo, c_hi;        // global kept indices of this batch
+    unsigned long long *d0;    // [V][dim] fixed-point deltas of syn0
+    unsigned long long *d1;    // [V-1][dim] of syn1
+    int32_t *flag0, *flag1;    // touched rows
+    int32_t *list0, *list1;
+    int32_t *cnt;              // [2] list lengths
+    unsigned long long *stats; // kept, pairs, nodes
+};
+
+namespace {
+
+__device__ __forceinline__ unsigned long long to_fixed(double v) {
+    return static_cast<unsigned long long>(__double2ll_rn(ldexp(v, kFrac)));
+}
+
+__device__ __forceinline__ void touch(int32_t *flag, int32_t *list, int32_t *cnt, int32_t r) {
+    if (atomicExch(&flag[r], 1) == 0) list[atomicAdd(cnt, 1)] = r;
+}
+
+template <int NE>
+__global__ __launch_bounds__(256) void k_sync_grad(SyncArgs a) {
+    const int lane = lane_id();
+    const int64_t gi = a.c_lo + (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
+    if (gi >= a.c_hi) return;
+    // document of kept centre gi: last d with kept_off[d] <= gi
+    int64_t lo = 0, hi = a.n_docs - 1;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (a.kept_off[mid] <= gi) lo = mid; else hi = mid - 1;
+    }
+    const int64_t d = lo;
+    const int j = static_cast<int>(gi - a.kept_off[d]);
+    const int nk = a.doc_kept[d];
+    const int64_t base = d * a.doc_len;
+    const uint32_t meta = a.kept_meta[base + j];
+    const int v = a.kept_vid[base + j];
+    const int eff = static_cast<int>(meta >> 16);
+    const int clo = max(0, j - eff), chi = min(nk - 1, j + eff);
+    const int P = chi - clo;
+    const int len = a.codelen[v];
+    if (lane == 0) {
+        atomicAdd(&a.stats[0], 1ull);
+        atomicAdd(&a.stats[1], static_cast<unsigned long long>(P));
+        atomicAdd(&a.stats[2], static_cast<unsigned long long>(P) * len);
+    }
+    if (P == 0) return;
+    const int64_t g = a.epoch_base + a.first_raw + base + static_cast<int64_t>(meta & 0xFFFFu);
+    const float alpha = a.alpha_tab[g / 10000 - a.blk0];
+    const uint64_t code = a.code[v];
+    const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
+    for (int p = 0; p < P; ++p) {
+        const int c = clo + p + ((clo + p >= j) ? 1 : 0);
+        const int w = a.kept_vid[base + c];
+        float x[NE];
+#pragma unroll
+        for (int i = 0; i < NE; ++i) {
+            const int col = lane + i * kWave;
+            x[i] = col < a.dim ? a.syn0[static_cast<int64_t>(w) * a.stride + col] : 0.0f;
+        }
+        for (int jn = 0; jn < len; ++jn) {
+            const int n = __builtin_amdgcn_readlane(my_pt, jn);
+            const float t = static_cast<float>((code >> jn) & 1ull);
+            float y[NE];
+            float s = 0.0f;
+#pragma unroll
+            for (int i = 0; i < NE; ++i) {
+                const int col = lane + i * kWave;
+                y[i] = col < a.dim ? a.syn1[static_cast<int64_t>(n) * a.stride + col] : 0.0f;
+                s = fmaf(x[i], y[i], s);
+            }
+            const float z = wave_sum(s);
+            const float f = 1.0f / (1.0f + expf(-z));
+            const float gr = (1.0f - t - f) * alpha;
+            if (lane == 0) touch(a.flag1, a.list1, a.cnt + 1, n);
+#pragma unroll
+            for (int i = 0; i < NE; ++i) {
+                const int col = lane + i * kWave;
+                if (col < a.dim) {
+                    atomicAdd(&a.d1[static_cast<int64_t>(n) * a.dim + col],
+                              to_fixed(static_cast<double>(gr) * static_cast<double>(x[i])));
+                    atomicAdd(&a.d0[static_cast<int64_t>(w) * a.dim + col],
+                              to_fixed(static_cast<double>(gr) * static_cast<double>(y[i])));
+                }
+            }
+        }
+        if (lane == 0) touch(a.flag0, a.list0, a.cnt, w);
+    }
+}
+
+// one wave per touched row: row += (float)(delta 2^-40); clear delta and flag
+__global__ __launch_bounds__(256) void k_sync_apply(float *w, int32_t stride, int32_t dim, unsigned long long *dl,
+                                                    int32_t *flag, const int32_t *list, const int32_t *cnt) {
+    const int lane = lane_id();
+    const int n = *cnt;
+    const int nw = gridDim.x * blockDim.x / kWave;
+    for (int k = (blockIdx.x * blockDim.x + threadIdx.x) / kWave; k < n; k += nw) {
+        const int r = list[k];
+        for (int col = lane; col < dim; col += kWave) {
+            unsigned long long *q = &dl[static_cast<int64_t>(r) * dim + col];
+            const double dv = ldexp(static_cast<double>(static_cast<long long>(*q)), -kFrac);
+            float *x = &w[static_cast<int64_t>(r) * stride + col];
+            *x = *x + static_cast<float>(dv);
+            *q = 0ull;
+        }
+        if (lane == 0) flag[r] = 0;
+    }
+}
+
+__global__ void k_reset_counts(int32_t *cnt) {
+    if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
+}
+
+__global__ void k_zero_u64_range(unsigned long long *p, int64_t n) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0;
+}
+__global__ void k_zero_i32_range(int32_t *p, int64_t n) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0;
+}
+
+__global__ __launch_bounds__(1024) void k_scan_kept(const int32_t *__restrict__ in, int64_t n,
+                                                    int64_t *__restrict__ out) {
+    __shared__ int64_t wsum[16];
+    __shared__ int64_t carry;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    for (int64_t base = 0; base < n; base += 1024) {
+        const int64_t i = base + threadIdx.x;
+        const int64_t x = i < n ? in[i] : 0;
+        int64_t inc = x;
+#pragma unroll
+        for (int dd = 1; dd < 64; dd <<= 1) {
+            const int64_t y = __shfl_up(inc, dd, 64);
+            if (lane >= dd) inc += y;
+        }
+        if (lane == 63) wsum[wid] = inc;
+        __syncthreads();
+        int64_t before = carry;
+        for (int w = 0; w < wid; ++w) before += wsum[w];
+        if (i < n) out[i] = before + inc - x;
+        __syncthreads();
+        if (threadIdx.x == 1023) carry = before + inc;
+        __syncthreads();
+    }
+}
+
+using SyncFn = void (*)(SyncArgs);
+SyncFn pick_sync(int dim) {
+    const int ne = (dim + kWave - 1) / kWave;
+    if (ne <= 1) return k_sync_grad<1>;
+    if (ne <= 2) return k_sync_grad<2>;
+    if (ne <= 4) return k_sync_grad<4>;
+    if (ne <= 5) return k_sync_grad<5>;
+    if (ne <= 8) return k_sync_grad<8>;
+    return k_sync_grad<16>;
+}
+
+}  // namespace
+
+size_t sync_extra_bytes(int32_t V, int32_t dim, int64_t n_docs) {
+    Carve c;
+    c.take<int64_t>(static_cast<size_t>(n_docs));                        // kept_off
+    c.take<unsigned long long>(static_cast<size_t>(V) * dim);            // d0
+    c.take<unsigned long long>(static_cast<size_t>(V) * dim);            // d1
+    c.take<int32_t>(static_cast<size_t>(V) * 4);                         // flags, lists
+    c.take<int32_t>(2);
+    return c.used();
+}
+
+int run_train_sync(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
+                   const float *alpha_tab, int64_t blk0, unsigned long long *tstats, hipStream_t s) {
+    const int64_t n_docs = std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len));
+    SyncArgs a{};
+    a.syn0 = m->syn0;
+    a.syn1 = m->syn1;
+    a.V = m->V;
+    a.dim = m->dim;
+    a.stride = m->row_stride;
+    a.codelen = m->codelen;
+    a.code = m->code;
+    a.point_off = m->point_off;
+    a.points = m->points;
+    a.kept_vid = b.kept_vid;
+    a.kept_meta = b.kept_meta;
+    a.doc_kept = b.doc_kept;
+    int64_t *kept_off = c.take<int64_t>(static_cast<size_t>(n_docs));
+    a.kept_off = kept_off;
+    a.n_docs = ceil_div(n_tokens, p->doc_len);
+    a.doc_len = p->doc_len;
+    a.first_raw = p->first_raw_index;
+    a.epoch_base = static_cast<int64_t>(p->epoch) * p->corpus_tokens;
+    a.alpha_tab = alpha_tab;
+    a.blk0 = blk0;
+    a.d0 = c.take<unsigned long long>(static_cast<size_t>(m->V) * m->dim);
+    a.d1 = c.take<unsigned long long>(static_cast<size_t>(m->V) * m->dim);
+    int32_t *fl = c.take<int32_t>(static_cast<size_t>(m->V) * 4);
+    a.flag0 = fl;
+    a.flag1 = fl + m->V;
+    a.list0 = fl + 2 * static_cast<size_t>(m->V);
+    a.list1 = fl + 3 * static_cast<size_t>(m->V);
+    a.cnt = c.take<int32_t>(2);
+    a.stats = tstats;
+    const unsigned zg = static_cast<unsigned>(std::min<int64_t>(8192, ceil_div(static_cast<int64_t>(m->V) * m->dim, 256)));
+    k_zero_u64_range<<<zg, 256, 0, s>>>(a.d0, static_cast<int64_t>(m->V) * m->dim);
+    k_zero_u64_range<<<zg, 256, 0, s>>>(a.d1, static_cast<int64_t>(m->V) * m->dim);
+    k_zero_i32_range<<<static_cast<unsigned>(ceil_div(2LL * m->V, 256)), 256, 0, s>>>(fl, 2LL * m->V);
+    k_reset_counts<<<1, 64, 0, s>>>(a.cnt);
+    if (n_tokens <= 0) return W2V_OK;
+    k_scan_kept<<<1, 1024, 0, s>>>(b.doc_kept, a.n_docs, kept_off);
+    W2V_LAUNCH_CHECK("sync setup");
+    int64_t tot[4];
+    W2V_HIP(hipMemcpyAsync(tot, b.totals, sizeof(tot), hipMemcpyDeviceToHost, s));
+    W2V_HIP(hipStreamSynchronize(s));
+    const int64_t kept = tot[2];
+    SyncFn fn = pick_sync(m->dim);
+    const unsigned ag = static_cast<unsigned>(std::max(1, device_cu_count() * 4));
+    for (int64_t lo = 0; lo < kept; lo += p->sync_batch) {
+        a.c_lo = lo;
+        a.c_hi = std::min<int64_t>(kept, lo + p->sync_batch);
+        const unsigned g = static_cast<unsigned>(ceil_div(a.c_hi - a.c_lo, 4));
+        hipLaunchKernelGGL(fn, dim3(g), dim3(256), 0, s, a);
+        k_sync_apply<<<ag, 256, 0, s>>>(m->syn0, m->row_stride, m->dim, a.d0, a.flag0, a.list0, a.cnt);
+        k_sync_apply<<<ag, 256, 0, s>>>(m->syn1, m->row_stride, m->dim, a.d1, a.flag1, a.list1, a.cnt + 1);
+        k_reset_counts<<<1, 64, 0, s>>>(a.cnt);
+        W2V_LAUNCH_CHECK("sync batch");
+    }
+    return W2V_OK;
+}
+
+// ------------------------------------------------------------- log-likelihood
+namespace {
+
+__device__ __forceinline__ double log_sigmoid(double u) {
+    return u >= 0.0 ? -log1p(exp(-u)) : u - log1p(exp(u));
+}
+
+struct LLArgs {
+    const float *syn0;
+    const float *syn1;
+    int32_t dim, stride;
+    const uint8_t *codelen;
+    const uint64_t *code;
+    const int32_t *point_off;
+    const int32_t *points;
+    const int32_t *kept_vid;
+    const uint32_t *kept_meta;
+    const int32_t *doc_kept;
+    int64_t n_docs;
+    int32_t doc_len;
+    double *doc_ll;
+    int64_t *doc_nodes;
+};
+
+template <int NE>
+__global__ __launch_bounds__(256) void k_loglik(LLArgs a) {
+    const int lane = lane_id();
+    const int64_t wave0 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * blockDim.x / kWave;
+    for (int64_t d = wave0; d < a.n_docs; d += nwaves) {
+        const int nk = a.doc_kept[d];
+        const int64_t base = d * a.doc_len;
+        double acc = 0.0;
+        int64_t nodes = 0;
+        for (int j = 0; j < nk; ++j) {
+            const int v = a.kept_vid[base + j];
+            const int eff = static_cast<int>(a.kept_meta[base + j] >> 16);
+            const int clo = max(0, j - eff), chi = min(nk - 1, j + eff);
+            const int P = chi - clo;
+            const int len = a.codelen[v];
+            const uint64_t code = a.code[v];
+            const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
+            for (int p = 0; p < P; ++p) {
+                const int c = clo + p + ((clo + p >= j) ? 1 : 0);
+                const int w = a.kept_vid[base + c];
+                float x[NE];
+#pragma unroll
+                for (int i = 0; i < NE; ++i) {
+                    const int col = lane + i * kWave;
+                    x[i] = col < a.dim ? a.syn0[static_cast<int64_t>(w) * a.stride + col] : 0.0f;
+                }
+                float mine = 0.0f;   // lane jn keeps the dot product of node jn
+                for (int jn = 0; jn < len; ++jn) {
+                    const int n = __builtin_amdgcn_readlane(my_pt, jn);
+                    float s = 0.0f;
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) {
+                        const int col = lane + i * kWave;
+                        const float y = col < a.dim ? a.syn1[static_cast<int64_t>(n) * a.stride + col] : 0.0f;
+                        s = fmaf(x[i], y, s);
+                    }
+                    const float z = wave_sum(s);
+                    if (lane == jn) mine = z;
+                }
+                if (lane < len) {
+                    const double sign = ((code >> lane) & 1ull) ? -1.0 : 1.0;
+                    acc += log_sigmoid(sign * static_cast<double>(mine));
+                }
+                nodes += len;
+            }
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) {
+            a.doc_ll[d] = acc;
+            a.doc_nodes[d] = nodes;
+        }
+    }
+}
+
+// fixed-order sum of per-document partials
+__global__ __launch_bounds__(1024) void k_sum_docs(const double *__restrict__ ll, const int64_t *__restrict__ nodes,
+                                                   int64_t n, double *__restrict__ out_ll,
+                                                   int64_t *__restrict__ out_nodes) {
+    __shared__ double sl[1024];
+    __shared__ int64_t sn[1024];
+    double a = 0.0;
+    int64_t b = 0;
+    for (int64_t i = threadIdx.x; i < n; i += 1024) {
+        a += ll[i];
+        b += nodes[i];
+    }
+    sl[threadIdx.x] = a;
+    sn[threadIdx.x] = b;
+    __syncthreads();
+    for (int st = 512; st > 0; st >>= 1) {
+        if (threadIdx.x < st) {
+            sl[threadIdx.x] += sl[threadIdx.x + st];
+            sn[threadIdx.x] += sn[threadIdx.x + st];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        *out_ll = sl[0];
+        *out_nodes = sn[0];
+    }
+}
+
+using LLFn = void (*)(LLArgs);
+LLFn pick_ll(int dim) {
+    const int ne = (dim + kWave - 1) / kWave;
+    if (ne <= 1) return k_loglik<1>;
+    if (ne <= 2) return k_loglik<2>;
+    if (ne <= 4) return k_loglik<4>;
+    if (ne <= 5) return k_loglik<5>;
+    if (ne <= 8) return k_loglik<8>;
+    return k_loglik<16>;
+}
+
+}  // namespace
+
+size_t loglik_extra_bytes(int64_t n_docs) {
+    Carve c;
+    c.take<double>(static_cast<size_t>(n_docs));
+    c.take<int64_t>(static_cast<size_t>(n_docs));
+    c.take<double>(1);
+    c.take<int64_t>(1);
+    return c.used();
+}
+
+int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
+               double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, hipStream_t s) {
+    const int64_t n_docs = std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len));
+    LLArgs a{};
+    a.syn0 = m->syn0;
+    a.syn1 = m->syn1;
+    a.dim = m->dim;
+    a.stride = m->row_stride;
+    a.codelen = m->codelen;
+    a.code = m->code;
+    a.point_off = m->point_off;
+    a.points = m->points;
+    a.kept_vid = b.kept_vid;
+    a.kept_meta = b.kept_meta;
+    a.doc_kept = b.doc_kept;
+    a.n_docs = n_tokens > 0 ? ceil_div(n_tokens, p->doc_len) : 0;
+    a.doc_len = p->doc_len;
+    a.doc_ll = c.take<double>(static_cast<size_t>(n_docs));
+    a.doc_nodes = c.take<int64_t>(static_cast<size_t>(n_docs));
+    double *out = c.take<double>(1);
+    int64_t *out_nodes = c.take<int64_t>(1);
+    if (a.n_docs > 0) {
+        const unsigned grid =
+            static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_docs, 4), 16LL * device_cu_count()));
+        hipLaunchKernelGGL(pick_ll(m->dim), dim3(grid), dim3(256), 0, s, a);
+        W2V_LAUNCH_CHECK("k_loglik");
+        k_sum_docs<<<1, 1024, 0, s>>>(a.doc_ll, a.doc_nodes, a.n_docs, out, out_nodes);
+        W2V_LAUNCH_CHECK("k_sum_docs");
+    }
+    double hll = 0.0;
+    int64_t nn = 0;
+    int64_t tot[4] = {0, 0, 0, 0};
+    if (a.n_docs > 0) {
+        W2V_HIP(hipMemcpyAsync(&hll, out, sizeof(hll), hipMemcpyDeviceToHost, s));
+        W2V_HIP(hipMemcpyAsync(&nn, out_nodes, sizeof(nn), hipMemcpyDeviceToHost, s));
+    }
+    W2V_HIP(hipMemcpyAsync(tot, b.totals, sizeof(tot), hipMemcpyDeviceToHost, s));
+    W2V_HIP(hipStreamSynchronize(s));
+    *sum_ll_host = hll;
+    *n_pairs_host = tot[3];
+    if (n_nodes_host) *n_nodes_host = nn;
+    return W2V_OK;
+}
+
+}  // namespace w2v

@@ -1,0 +1,163 @@
+// Internal declarations shared by the library's translation units (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "../../include/w2v.h"
+
+namespace w2v {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- errors
+void set_error(const std::string &msg);
+int fail(int code, const std::string &msg);
+int hip_fail(hipError_t e, const char *what);
+
+#define W2V_HIP(call)                                            \
+    do {                                                         \
+        hipError_t _e = (call);                                  \
+        if (_e != hipSuccess) return ::w2v::hip_fail(_e, #call); \
+    } while (0)
+
+#define W2V_LAUNCH_CHECK(what)                                            \
+    do {                                                                  \
+        hipError_t _e = hipGetLastError();                                \
+        if (_e != hipSuccess) return ::w2v::hip_fail(_e, "launch " what); \
+    } while (0)
+
+// Bump allocator over the caller's workspace (256-byte aligned carving).
+struct Carve {
+    char *base;
+    size_t cap, off;
+    explicit Carve(void *p = nullptr, size_t c = 0) : base(static_cast<char *>(p)), cap(c), off(0) {}
+    template <class T>
+    T *take(size_t n) {
+        off = (off + 255) & ~size_t(255);
+        T *r = base ? reinterpret_cast<T *>(base + off) : nullptr;
+        off += n * sizeof(T);
+        return r;
+    }
+    size_t used() const { return (off + 255) & ~size_t(255); }
+};
+
+int device_cu_count();
+size_t device_max_lds();
+void record_train_launch(int groups, int waves);
+
+// ----------------------------------------------------------- device helpers
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): counter (c0..c3), key (k0, k1).
+struct U4 {
+    uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ U4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                            uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+        const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+        const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return U4{c0, c1, c2, c3};
+}
+
+// The two words a raw token draws: .x decides the keep, .y the window.
+__device__ __forceinline__ U4 token_draw(uint64_t seed, int64_t raw, int32_t epoch) {
+    return philox4x32_10(static_cast<uint32_t>(raw), static_cast<uint32_t>(static_cast<uint64_t>(raw) >> 32),
+                         static_cast<uint32_t>(epoch), 0u, static_cast<uint32_t>(seed),
+                         static_cast<uint32_t>(seed >> 32));
+}
+
+__device__ __forceinline__ uint64_t fmix64(uint64_t k) {
+    k ^= k >> 33;
+    k *= 0xFF51AFD7ED558CCDull;
+    k ^= k >> 33;
+    k *= 0xC4CEB9FE1A85EC53ull;
+    k ^= k >> 33;
+    return k;
+}
+
+__device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x & (kWave - 1)); }
+
+// Full-wave sum, result in every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+    return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+    return v;
+}
+__device__ __forceinline__ int64_t wave_sum(int64_t v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+    return v;
+}
+
+// ---------------------------------------------------------- sampling layout
+// Per document d, slots [d*doc_len, d*doc_len + n_kept[d]) of:
+//   kept_vid  int32   vocabulary index of the kept token
+//   kept_meta uint32  raw offset in the document (bits 0..15) | effective half-width (bits 16..23)
+struct SampleBufs {
+    int32_t *kept_vid;
+    uint32_t *kept_meta;
+    int32_t *doc_kept;     // [n_docs]
+    int64_t *doc_pairs;    // [n_docs]
+    uint64_t *thr;         // [V]
+    int64_t *totals;       // [4]: raw, in-vocab, kept, pairs
+};
+
+size_t sample_bufs_bytes(int32_t V, int64_t n_tokens, int32_t doc_len);
+SampleBufs sample_bufs_carve(Carve &c, int32_t V, int64_t n_tokens, int32_t doc_len);
+
+// Launches: thresholds, zero totals, per-document subsampling + window draws.
+int launch_sampling(const int32_t *tokens, int64_t n_tokens, int32_t V, const int64_t *vocab_counts,
+                    int64_t train_words, const w2v_params *p, const SampleBufs &b, uint8_t *keep_mask,
+                    hipStream_t s);
+int launch_thresholds(const int64_t *vocab_counts, int32_t V, double sample, int64_t train_words, uint64_t *thr,
+                      hipStream_t s);
+
+// Learning-rate table: alpha of 10,000-token blocks [blk0, blk0 + nblk).
+int launch_alpha_table(const w2v_params *p, int64_t blk0, int64_t nblk, float *tab, hipStream_t s);
+
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Arguments of the asynchronous training kernel.
+struct TrainArgs {
+    float *syn0;
+    float *syn1;
+    int32_t V, dim, stride;
+    const uint8_t *codelen;
+    const uint64_t *code;
+    const int32_t *point_off;
+    const int32_t *points;
+    const int32_t *kept_vid;
+    const uint32_t *kept_meta;
+    const int32_t *doc_kept;
+    int64_t n_docs;
+    int32_t doc_len;
+    int64_t first_raw;
+    int64_t epoch_base;      // epoch * corpus_tokens
+    const float *alpha_tab;
+    int64_t blk0;
+    int32_t cache_k, cache_first, flush_every;
+    int32_t workers;
+    int32_t write_policy;
+    float flush_scale;       // fraction of the cached rows' change written back (1 = all of it)
+    int32_t *queue;
+    unsigned long long *stats;   // [3]: kept, pairs, node updates
+};
+
+}  // namespace w2v

@@ -1,0 +1,54 @@
+"""Shared set-up for the GPU parity tests: one workload, both sides."""
+from __future__ import annotations
+
+import functools
+import sys
+from dataclasses import dataclass
+
+import numpy as np
+
+import oracle
+import synth
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@functools.lru_cache(maxsize=4)
+def corpus(name: str, n_tokens: int | None = None, heldout: bool = False) -> np.ndarray:
+    w = synth.WORKLOADS[name]
+    if n_tokens is not None:
+        w = w.scaled(n_tokens)
+    return synth.workload_corpus(w, heldout=heldout, threads=16)
+
+
+@dataclass
+class Side:
+    """The oracle's view of a workload."""
+    w: synth.Workload
+    tok: np.ndarray
+    voc: oracle.Vocab
+    tree: oracle.Tree
+    tv: np.ndarray
+
+
+@functools.lru_cache(maxsize=4)
+def oracle_side(name: str, n_tokens: int | None = None) -> Side:
+    w = synth.WORKLOADS[name]
+    if n_tokens is not None:
+        w = w.scaled(n_tokens)
+    tok = corpus(name, n_tokens)
+    voc = oracle.build_vocab(tok, w.vocab, w.min_count)
+    tree = oracle.build_huffman(voc.vocab_counts)
+    tv = oracle.remap(tok, voc.id_to_vocab)
+    return Side(w, tok, voc, tree, tv)
+
+
+def row_rel_err(a: np.ndarray, b: np.ndarray) -> float:
+    """max over rows of ||a_r - b_r||_inf / ||b_r||_inf (rows where b_r == 0 use the absolute error)."""
+    d = np.abs(a.astype(np.float64) - b.astype(np.float64)).max(axis=1)
+    s = np.abs(b.astype(np.float64)).max(axis=1)
+    r = np.where(s > 0, d / np.where(s > 0, s, 1), d)
+    return float(r.max()) if r.size else 0.0

@@ -1,0 +1,142 @@
+"""The C-ABI library: it loads, exports every symbol include/w2v.h declares, the
+binding's structs match the header, and argument errors are reported before
+anything is launched (no GPU needed for these)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "w2v.h")
+
+
+@pytest.fixture(scope="module")
+def w2v():
+    import paper_1606_07822_amd as w2v
+    if not os.path.exists(w2v.LIB_PATH):
+        pytest.skip("libw2v.so not built")
+    return w2v
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(w2v_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for n in ("w2v_build_vocab", "w2v_build_huffman", "w2v_train_hs_epoch", "w2v_hs_loglik"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(w2v):
+    lib = ctypes.CDLL(w2v.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_struct_layouts_match_header(w2v):
+    # offsets the header implies (natural alignment, LP64)
+    assert w2v.CModel.V.offset == 16 and w2v.CModel.vocab_counts.offset == 32
+    assert w2v.CModel.points.offset == 72 and ctypes.sizeof(w2v.CModel) == 80
+    assert w2v.CParams.sample.offset == 16 and w2v.CParams.corpus_tokens.offset == 40
+    assert w2v.CParams.seed.offset == 56 and w2v.CParams.write_policy.offset == 80
+    assert ctypes.sizeof(w2v.CParams) == 112
+
+
+def test_vocab_argument_errors(w2v):
+    L = w2v.lib()
+    V = ctypes.c_int32(0)
+    tw = ctypes.c_int64(0)
+    fake = ctypes.c_void_p(0x1000)
+    rc = L.w2v_build_vocab(fake, 10, 0, 5, fake, fake, fake, fake, None, ctypes.byref(V), ctypes.byref(tw), fake, 1 << 20,
+                           None)
+    assert rc == w2v.W2V_E_ARG and "id_space" in w2v.last_error()
+    rc = L.w2v_build_vocab(fake, -1, 10, 5, fake, fake, fake, fake, None, ctypes.byref(V), ctypes.byref(tw), fake,
+                           1 << 20, None)
+    assert rc == w2v.W2V_E_ARG
+    rc = L.w2v_build_vocab(fake, 10, 10, 5, fake, fake, fake, fake, None, ctypes.byref(V), ctypes.byref(tw), fake, 8,
+                           None)
+    assert rc == w2v.W2V_E_WORKSPACE and "workspace" in w2v.last_error()
+    rc = L.w2v_build_vocab(fake, 10, 10, 5, fake, fake, fake, fake, fake, ctypes.byref(V), ctypes.byref(tw), fake,
+                           1 << 20, None)
+    assert rc == w2v.W2V_E_ARG and "alias" in w2v.last_error()
+
+
+def test_huffman_argument_errors(w2v):
+    L = w2v.lib()
+    fake = ctypes.c_void_p(0x1000)
+    a = ctypes.c_int64(0)
+    b = ctypes.c_int32(0)
+    assert L.w2v_build_huffman(fake, 1, fake, fake, fake, None, 0, ctypes.byref(a), ctypes.byref(b), fake, 1 << 20,
+                               None) == w2v.W2V_E_ARG
+    need = L.w2v_build_huffman_workspace_bytes(1000)
+    assert need > 1000 * (8 + 8)
+    assert L.w2v_build_huffman(fake, 1000, fake, fake, fake, None, 0, ctypes.byref(a), ctypes.byref(b), fake, need - 1,
+                               None) == w2v.W2V_E_WORKSPACE
+
+
+def _model(w2v, **kw):
+    m = w2v.CModel(0x1000, 0x2000, 100, 50, 64, 0, 0x3000, 1000, 0x4000, 0x5000, 0x6000, 0x7000)
+    for k, v in kw.items():
+        setattr(m, k, v)
+    return m
+
+
+def _params(w2v, **kw):
+    p = w2v.Params(window=5, corpus_tokens=1000).c()
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+@pytest.mark.parametrize("mk,pk,msg", [
+    (dict(V=1), {}, "V must"),
+    (dict(dim=0), {}, "dim"),
+    (dict(dim=2000, row_stride=2000), {}, "dim"),
+    (dict(row_stride=49), {}, "row_stride"),
+    (dict(row_stride=66), {}, "row_stride"),
+    (dict(syn0=0x1004), {}, "aligned"),
+    (dict(points=0), {}, "Huffman"),
+    ({}, dict(window=0), "window"),
+    ({}, dict(window=11), "window"),
+    ({}, dict(doc_len=0), "doc_len"),
+    ({}, dict(sample=1.5), "sample"),
+    ({}, dict(first_raw_index=7), "first_raw_index"),
+    ({}, dict(arch=2), "arch"),
+    ({}, dict(mode=1, arch=1), "synchronous"),
+    ({}, dict(epoch=1, n_epochs=1), "epoch"),
+    ({}, dict(flush_every=0), "flush_every"),
+    ({}, dict(cache_k=-1), "cache_k"),
+    ({}, dict(cache_k=100), "cache_k"),
+    ({}, dict(alpha0=0.0), "alpha0"),
+])
+def test_train_argument_errors(w2v, mk, pk, msg):
+    L = w2v.lib()
+    m = _model(w2v, **mk)
+    p = _params(w2v, **pk)
+    rc = L.w2v_train_hs_epoch(ctypes.byref(m), ctypes.c_void_p(0x8000), 1000, ctypes.byref(p), None,
+                              ctypes.c_void_p(0x9000), 1 << 40, None)
+    assert rc == w2v.W2V_E_ARG
+    assert msg in w2v.last_error()
+
+
+def test_workspace_queries_grow_with_input(w2v):
+    m = _model(w2v)
+    p = _params(w2v)
+    L = w2v.lib()
+    a = L.w2v_train_workspace_bytes(ctypes.byref(m), 10_000, ctypes.byref(p))
+    b = L.w2v_train_workspace_bytes(ctypes.byref(m), 1_000_000, ctypes.byref(p))
+    assert 0 < a < b
+    ps = _params(w2v, mode=1)
+    assert L.w2v_train_workspace_bytes(ctypes.byref(m), 10_000, ctypes.byref(ps)) > a
+    assert L.w2v_hs_loglik_workspace_bytes(ctypes.byref(m), 10_000, ctypes.byref(p)) > 0
+    assert L.w2v_sample_pairs_workspace_bytes(100, 10_000, ctypes.byref(p)) > 0
+
+
+def test_binding_refuses_host_tensors(w2v):
+    import torch
+    with pytest.raises(ValueError):
+        w2v.build_vocab(torch.zeros(10, dtype=torch.int32), 10)

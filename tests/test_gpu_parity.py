@@ -1,0 +1,339 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Integer work (counts, vocabulary order, Huffman codes/points, keep thresholds,
+sampled pairs) must match bit for bit. Floating-point work: synchronous-mode
+embeddings within 1e-4 (row-wise relative, ∞-norm), a single sequential
+worker within 1e-4 of the oracle's centre-major order, evaluation
+log-likelihood within 1e-6 relative on the same model, and asynchronous
+training's held-out log-likelihood within 1 % of the oracle's.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_common import corpus, log, oracle_side, row_rel_err
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def w2v():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1606_07822_amd as w2v
+    w2v.lib()
+    return w2v
+
+
+@pytest.fixture(scope="module")
+def torch_mod():
+    import torch
+    return torch
+
+
+def to_dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def gpu_side(w2v, side):
+    voc = w2v.build_vocab(to_dev(side.tok), side.w.vocab, side.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    return voc, tree
+
+
+# ------------------------------------------------------------- vocabulary
+@pytest.mark.parametrize("name,n", [("tiny_sg_v1k_d50", None), ("sg_v30k_d100", None), ("sg_v100k_d200", None)])
+def test_vocab_bit_exact(w2v, name, n):
+    log(f"vocab {name}")
+    s = oracle_side(name, n)
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    assert voc.V == s.voc.V and voc.train_words == s.voc.train_words
+    np.testing.assert_array_equal(voc.counts_by_id.cpu().numpy(), s.voc.counts)
+    np.testing.assert_array_equal(voc.vocab_ids.cpu().numpy(), s.voc.vocab_ids)
+    np.testing.assert_array_equal(voc.vocab_counts.cpu().numpy(), s.voc.vocab_counts)
+    np.testing.assert_array_equal(voc.id_to_vocab.cpu().numpy(), s.voc.id_to_vocab)
+    np.testing.assert_array_equal(voc.tokens.cpu().numpy(), s.tv)
+
+
+@pytest.mark.parametrize("case", ["empty", "single_id", "min_count_0", "id_space_1", "ragged_big_space", "all_dropped"])
+def test_vocab_edge_cases(w2v, case):
+    rng = np.random.default_rng(5)
+    id_space, mc = 1000, 5
+    if case == "empty":
+        tok = np.zeros(0, np.int32)
+    elif case == "single_id":
+        tok = np.full(777, 3, np.int32)
+    elif case == "min_count_0":
+        tok = rng.integers(0, 50, 300).astype(np.int32); mc = 0
+    elif case == "id_space_1":
+        tok = np.zeros(100, np.int32); id_space = 1
+    elif case == "ragged_big_space":
+        id_space = 3_000_017
+        tok = (rng.zipf(1.1, 2_000_003) % id_space).astype(np.int32)
+    else:
+        tok = np.arange(1000, dtype=np.int32)
+    voc = w2v.build_vocab(to_dev(tok) if tok.size else to_dev(np.zeros(1, np.int32))[:0], id_space, mc)
+    o = oracle.build_vocab(tok, id_space, mc)
+    assert voc.V == o.V and voc.train_words == o.train_words
+    np.testing.assert_array_equal(voc.counts_by_id.cpu().numpy(), o.counts)
+    np.testing.assert_array_equal(voc.vocab_ids.cpu().numpy(), o.vocab_ids)
+    np.testing.assert_array_equal(voc.id_to_vocab.cpu().numpy(), o.id_to_vocab)
+
+
+def test_vocab_out_of_range_token_is_an_error(w2v):
+    tok = np.array([0, 1, 2, 5000, 3], np.int32)
+    with pytest.raises(w2v.W2VError) as e:
+        w2v.build_vocab(to_dev(tok), 1000, 1)
+    assert e.value.code == w2v.W2V_E_RANGE
+
+
+# ------------------------------------------------------------- Huffman
+def check_tree(w2v, counts):
+    t = w2v.build_huffman(to_dev(counts))
+    o = oracle.build_huffman(counts)
+    np.testing.assert_array_equal(t.codelen.cpu().numpy(), o.codelen)
+    np.testing.assert_array_equal(t.code.cpu().numpy().view(np.uint64), o.code)
+    np.testing.assert_array_equal(t.point_off.cpu().numpy(), o.point_off)
+    np.testing.assert_array_equal(t.points.cpu().numpy(), o.points)
+    assert t.max_len == int(o.codelen.max())
+
+
+@pytest.mark.parametrize("V,hi,seed", [(2, 10, 0), (3, 3, 1), (17, 5, 2), (1000, 4, 3), (4097, 100, 4),
+                                       (50_000, 20, 5), (50_000, 10**6, 6)])
+def test_huffman_random_counts_bit_exact(w2v, V, hi, seed):
+    rng = np.random.default_rng(seed)
+    check_tree(w2v, np.sort(rng.integers(1, hi, V))[::-1].astype(np.int64))
+
+
+def test_huffman_equal_counts(w2v):
+    check_tree(w2v, np.full(1 << 12, 9, np.int64))
+    check_tree(w2v, np.full(5000, 5, np.int64))
+
+
+@pytest.mark.parametrize("V,s,N", [(30_000, 1.0, 10**7), (100_000, 1.0, 10**8), (1_000_000, 1.05, 10**9)])
+def test_huffman_zipf_vocab_bit_exact(w2v, V, s, N):
+    log(f"huffman zipf V={V}")
+    p = synth.zipf_probs(V, s)
+    counts = np.maximum(np.floor(p * N), 5).astype(np.int64)
+    counts = np.sort(counts)[::-1].copy()
+    check_tree(w2v, counts)
+
+
+def test_huffman_too_deep_is_an_error(w2v):
+    fib = [1, 1]
+    while len(fib) < 70:
+        fib.append(fib[-1] + fib[-2])
+    with pytest.raises(w2v.W2VError) as e:
+        w2v.build_huffman(to_dev(np.array(sorted(fib, reverse=True), np.int64)))
+    assert e.value.code == w2v.W2V_E_RANGE
+
+
+# ------------------------------------------------------------- sampling
+@pytest.mark.parametrize("name,t", [("sg_v30k_d100", 1e-3), ("sg_v100k_d200", 1e-4), ("sg_v100k_d200", 1e-5)])
+def test_keep_thresholds_bit_exact(w2v, name, t):
+    s = oracle_side(name)
+    thr = w2v.keep_thresholds(to_dev(s.voc.vocab_counts), t, s.voc.train_words).cpu().numpy().view(np.uint64)
+    np.testing.assert_array_equal(thr, oracle.keep_thresholds(s.voc.vocab_counts, t, s.voc.train_words))
+
+
+def pairs_both(w2v, s, tv, **kw):
+    p = w2v.Params(window=kw.get("window", s.w.window), sample=kw.get("sample", s.w.sample),
+                   doc_len=kw.get("doc_len", 1000), seed=kw.get("seed", 3), epoch=kw.get("epoch", 0),
+                   first_raw_index=kw.get("first", 0))
+    op = oracle.params(s.voc.V, 8, window=p.window, sample=p.sample, train_words=s.voc.train_words,
+                       doc_len=p.doc_len, seed=p.seed, epoch=p.epoch, first_raw_index=p.first_raw_index)
+    cap = kw.get("cap", None)
+    o = oracle.sample_pairs(tv, op, s.voc.vocab_counts, cap=cap)
+    g = w2v.sample_pairs(to_dev(tv), s.voc.V, to_dev(s.voc.vocab_counts), s.voc.train_words, p,
+                         cap=o.total if cap is None else cap, want_mask=True)
+    return o, g
+
+
+@pytest.mark.parametrize("name,n,kw", [
+    ("tiny_sg_v1k_d50", None, {}),
+    ("tiny_sg_v1k_d50", None, dict(window=1)),
+    ("tiny_sg_v1k_d50", None, dict(window=10, doc_len=333)),
+    ("sg_v30k_d100", 2_000_500, {}),                     # ragged last document
+    ("sg_v30k_d100", 2_000_000, dict(first=7_000_000, epoch=2, seed=11)),
+])
+def test_pairs_bit_exact(w2v, name, n, kw):
+    s = oracle_side(name)
+    tv = s.tv[:n] if n else s.tv
+    o, g = pairs_both(w2v, s, tv, **kw)
+    assert g.total == o.total and g.n_kept == o.n_kept and g.checksum == o.checksum
+    np.testing.assert_array_equal(g.keep_mask.cpu().numpy(), o.keep_mask)
+    np.testing.assert_array_equal(g.centre.cpu().numpy(), o.centre)
+    np.testing.assert_array_equal(g.context.cpu().numpy(), o.context)
+
+
+@pytest.mark.parametrize("name", ["sg_v30k_d100", "sg_v100k_d200"])
+def test_pairs_checksum_full_corpus(w2v, name):
+    log(f"pairs checksum {name}")
+    s = oracle_side(name)
+    o, g = pairs_both(w2v, s, s.tv, cap=0)
+    assert (g.total, g.n_kept, g.checksum) == (o.total, o.n_kept, o.checksum)
+
+
+# ------------------------------------------------------------- evaluation
+def test_loglik_matches_oracle_on_the_same_model(w2v):
+    s = oracle_side("sg_v30k_d100")
+    voc, tree = gpu_side(w2v, s)
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim, syn1_scale=0.3)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    held = corpus("sg_v30k_d100", heldout=True)
+    hv = oracle.remap(held, s.voc.id_to_vocab)
+    p = w2v.Params(window=5, sample=1e-3, seed=synth.SEED_EVAL)
+    sg, npg, nng = w2v.hs_loglik(model, to_dev(hv), p)
+    op = oracle.params(s.voc.V, s.w.dim, window=5, sample=1e-3, train_words=s.voc.train_words, seed=synth.SEED_EVAL)
+    so, npo, nno = oracle.loglik(syn0, syn1, s.tree, hv, op)
+    assert (npg, nng) == (npo, nno)
+    assert abs(sg - so) <= 1e-6 * abs(so)
+
+
+def test_loglik_at_zero_syn1_closed_form(w2v):
+    s = oracle_side("tiny_sg_v1k_d50")
+    voc, tree = gpu_side(w2v, s)
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    sg, npairs, nnodes = w2v.hs_loglik(model, voc.tokens, w2v.Params(window=2, seed=4))
+    assert npairs > 0
+    assert abs(sg + math.log(2.0) * nnodes) <= 1e-9 * nnodes
+
+
+# ------------------------------------------------------------- synchronous mode
+# Batches of >= 1024 centres at alpha 0.025 diverge within ten batches (the oracle too: the top
+# inner nodes take the whole batch's gradient at once), so the ten-batch cases use 256 centres.
+@pytest.mark.parametrize("name,n,batches,B", [("tiny_sg_v1k_d50", None, 1, 4096), ("tiny_sg_v1k_d50", None, 10, 256),
+                                              ("sg_v30k_d100", 1_000_000, 1, 4096),
+                                              ("sg_v30k_d100", 1_000_000, 10, 256),
+                                              ("tiny_sg_v1k_d50", 20_000, 3, 1)])
+def test_sync_mode_within_1e4(w2v, name, n, batches, B):
+    log(f"sync {name} batches={batches}")
+    s = oracle_side(name)
+    nk_needed = batches * B
+    # the token prefix holding exactly `batches` batches of kept centres (whole documents past it are cut)
+    tv = s.tv if n is None else s.tv[:n]
+    voc, tree = gpu_side(w2v, s)
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim, syn1_scale=0.5 / s.w.dim)
+    # GPU runs every batch of tv; the oracle stops after `batches`: cut tv so both see the same batches
+    op = oracle.params(s.voc.V, s.w.dim, window=s.w.window, sample=s.w.sample, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, sync_batch=B)
+    pr = oracle.sample_pairs(tv, op, s.voc.vocab_counts, cap=0)
+    kept_prefix = np.cumsum(pr.keep_mask)
+    cut = int(np.searchsorted(kept_prefix, nk_needed)) + 1 if kept_prefix[-1] > nk_needed else tv.size
+    tv = tv[:cut]
+    a0, a1 = syn0.copy(), syn1.copy()
+    ost = oracle.train_sync(a0, a1, s.tree, tv, op, n_batches=-1)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=s.w.window, sample=s.w.sample, corpus_tokens=s.tv.size, mode=1, sync_batch=B)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    g1 = g1[:s.voc.V - 1]
+    assert row_rel_err(g0, a0) <= 1e-4
+    assert row_rel_err(g1, a1) <= 1e-4
+    # rows no pair touched are bit-identical
+    np.testing.assert_array_equal(g0[(a0 == syn0).all(1)], syn0[(a0 == syn0).all(1)])
+
+
+def test_sync_mode_is_deterministic(w2v):
+    s = oracle_side("tiny_sg_v1k_d50")
+    voc, tree = gpu_side(w2v, s)
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim, syn1_scale=0.01)
+    outs = []
+    for _ in range(2):
+        model = w2v.make_model(syn0, syn1, voc, tree)
+        w2v.train_hs_epoch(model, voc.tokens, w2v.Params(window=2, corpus_tokens=s.tv.size, mode=1, sync_batch=512))
+        outs.append([t.cpu().numpy() for t in model.vectors()])
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
+# ------------------------------------------------------------- asynchronous mode
+@pytest.mark.parametrize("arch,k,F,ndocs", [(0, 0, 10, 5), (0, 31, 10, 5), (0, 7, 1, 5), (1, 0, 10, 5),
+                                             (1, 31, 10, 5)])
+def test_single_worker_matches_oracle_centre_major(w2v, arch, k, F, ndocs):
+    s = oracle_side("sg_v30k_d100")
+    voc, tree = gpu_side(w2v, s)
+    tv = s.tv[:ndocs * 1000]
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim, syn1_scale=0.5 / s.w.dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    alpha0 = 0.05 if arch else 0.025
+    op = oracle.params(s.voc.V, s.w.dim, window=5, sample=1e-3, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, cache_k=k, flush_every=F, order=1, arch=arch, alpha0=alpha0)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, cache_k=k, flush_every=F, workers=1, arch=arch,
+                   alpha0=alpha0)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4
+    assert row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+def async_ll(w2v, s, held, **kw):
+    voc, tree = gpu_side(w2v, s)
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=s.w.window, sample=s.w.sample, corpus_tokens=s.tv.size, arch=s.w.arch, alpha0=s.w.alpha0,
+                   **kw)
+    w2v.train_hs_epoch(model, voc.tokens, p)
+    hv = to_dev(oracle.remap(held, s.voc.id_to_vocab))
+    sg, npairs, _ = w2v.hs_loglik(model, hv, w2v.Params(window=s.w.window, sample=s.w.sample, seed=synth.SEED_EVAL))
+    return sg / npairs, npairs
+
+
+@pytest.mark.parametrize("kw", [dict(cache_k=0), dict(cache_k=31, flush_every=10, flush_policy=0),
+                                dict(cache_k=31)])
+def test_async_loglik_within_1pct_tiny(w2v, kw):
+    s = oracle_side("tiny_sg_v1k_d50")
+    held = corpus("tiny_sg_v1k_d50", heldout=True)
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim)
+    op = oracle.params(s.voc.V, s.w.dim, window=2, train_words=s.voc.train_words, corpus_tokens=s.tv.size,
+                       cache_k=31, flush_every=10)
+    oracle.train(syn0, syn1, s.tree, s.tv, op)
+    hv = oracle.remap(held, s.voc.id_to_vocab)
+    so, npo, _ = oracle.loglik(syn0, syn1, s.tree, hv, oracle.params(s.voc.V, s.w.dim, window=2,
+                                                                      train_words=s.voc.train_words, seed=4))
+    g, npg = async_ll(w2v, s, held, **kw)
+    assert npg == npo
+    assert abs(g - so / npo) <= 0.01 * abs(so / npo), (g, so / npo)
+
+
+def golden(name):
+    path = os.path.join(GOLDEN, f"oracle_ll_{name}.json")
+    if not os.path.exists(path):
+        pytest.skip(f"no stored oracle result {path}")
+    return json.load(open(path))
+
+
+# Default asynchronous mode (top-31 cache in LDS, write-back of the workgroups' averaged change every
+# 1000 centres, atomic adds elsewhere) at full occupancy; the uncached Hogwild store policy; and the
+# cache with the paper's summed write-back, which is stable only at low concurrency (256 wavefronts).
+@pytest.mark.parametrize("name,kw", [
+    ("sg_v30k_d100", {}),
+    ("sg_v30k_d100", dict(cache_k=0, write_policy=1)),
+    ("sg_v30k_d100", dict(workers=256, cache_k=31, flush_every=10, flush_policy=0)),
+    ("sg_v100k_d200", {}),
+    ("cbow_v100k_d300", {}),
+])
+def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw):
+    log(f"async LL {name} {kw}")
+    gold = golden(name)
+    s = oracle_side(name)
+    assert s.voc.V == gold["V"] and s.voc.train_words == gold["train_words"]
+    held = corpus(name, heldout=True)
+    g, npg = async_ll(w2v, s, held, **kw)
+    assert npg == gold["heldout_pairs"]
+    ref = gold["mean_ll"]
+    log(f"  gpu {g:.6f} oracle {ref:.6f} init {gold['init_mean_ll']:.6f}")
+    assert abs(g - ref) <= 0.01 * abs(ref)
