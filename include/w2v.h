@@ -131,7 +131,9 @@ typedef struct {
     int32_t flush_every;     /* write the cache back after this many centre words per workgroup (>= 1) */
     int32_t sync_batch;      /* synchronous mode: kept centres per batch (>= 1) */
     int32_t workers;         /* wavefronts that take documents; 0 = fill the GPU; 1 = one sequential worker */
-    int32_t write_policy;    /* uncached inner nodes: 0 = atomic add of the change, 1 = plain store */
+    int32_t write_policy;    /* bit 0: uncached inner-node rows are stored (lock-free, concurrent updates may be
+                                overwritten, as in Hogwild) instead of atomically adding their change;
+                                bit 1: the same for the word vectors syn0 */
     int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), 1 = add the
                                 change divided by the number of workgroups (their progress averaged) */
     int32_t reserved2[6];

@@ -176,14 +176,11 @@ def build_huffman(vocab_counts: torch.Tensor) -> Tree:
     ws = _workspace(lib().w2v_build_huffman_workspace_bytes(V), dev)
     plen = ctypes.c_int64(0)
     mlen = ctypes.c_int32(0)
-    # one call with a points buffer of the largest possible size would waste memory; size first
+    # codes are at most 64 long: one call with a buffer of that bound builds the tree once
+    points = torch.empty(max(V * min(64, V - 1), 1), dtype=torch.int32, device=dev)
     _check(lib().w2v_build_huffman(_dev_ptr(vc, torch.int64, "vocab_counts"), V, codelen.data_ptr(),
-                                   code.data_ptr(), off.data_ptr(), None, 0, ctypes.byref(plen), ctypes.byref(mlen),
-                                   ws.data_ptr(), ws.numel(), _stream(dev)))
-    points = torch.empty(max(plen.value, 1), dtype=torch.int32, device=dev)
-    _check(lib().w2v_build_huffman(vc.data_ptr(), V, codelen.data_ptr(), code.data_ptr(), off.data_ptr(),
-                                   points.data_ptr(), points.numel(), ctypes.byref(plen), ctypes.byref(mlen),
-                                   ws.data_ptr(), ws.numel(), _stream(dev)))
+                                   code.data_ptr(), off.data_ptr(), points.data_ptr(), points.numel(),
+                                   ctypes.byref(plen), ctypes.byref(mlen), ws.data_ptr(), ws.numel(), _stream(dev)))
     return Tree(codelen, code, off, points[:plen.value], mlen.value)
 
 
@@ -253,7 +250,7 @@ class Params:
     flush_every: int = 1000
     sync_batch: int = 4096
     workers: int = 0
-    write_policy: int = 0
+    write_policy: int = 1
     flush_policy: int = 1
     extra: dict = field(default_factory=dict)
 

@@ -64,24 +64,28 @@ __global__ __launch_bounds__(64) void k_huff_merge(const int64_t *__restrict__ l
             while (a < V - 1) {
                 if (!leaf_ok(lf) || !leaf_ok(lf - 1)) { want = 1; break; }
                 if (!inner_ok(ih, a) || !inner_ok(ih + 1, a)) { want = 2; break; }
-                int64_t sum = 0;
-#pragma unroll
-                for (int pick = 0; pick < 2; ++pick) {
-                    bool use_leaf;
-                    if (lf < 0) use_leaf = false;
-                    else if (ih >= a) use_leaf = true;
-                    else use_leaf = leaf_at(lf) <= inner_at(ih, a);   // a leaf wins a tie
-                    int32_t child;
-                    if (use_leaf) {
-                        sum += leaf_at(lf);
-                        child = lf--;
-                    } else {
-                        sum += inner_at(ih, a);
-                        child = V + ih++;
-                    }
-                    parent[child] = a;
-                    bit[child] = static_cast<uint8_t>(pick);
-                }
+                // the two fronts of each queue, read together
+                const int64_t L0 = lf >= 0 ? leaf_at(lf) : 0;
+                const int64_t L1 = lf >= 1 ? leaf_at(lf - 1) : 0;
+                const int64_t I0 = ih < a ? inner_at(ih, a) : 0;
+                const int64_t I1 = ih + 1 < a ? inner_at(ih + 1, a) : 0;
+                // first child (bit 0): a leaf wins a tie
+                const bool t1 = lf >= 0 && (ih >= a || L0 <= I0);
+                const int32_t c1 = t1 ? lf : V + ih;
+                const int64_t v1 = t1 ? L0 : I0;
+                const int32_t lf2 = t1 ? lf - 1 : lf, ih2 = t1 ? ih : ih + 1;
+                const int64_t lv = t1 ? L1 : L0, iv = t1 ? I0 : I1;
+                // second child (bit 1)
+                const bool t2 = lf2 >= 0 && (ih2 >= a || lv <= iv);
+                const int32_t c2 = t2 ? lf2 : V + ih2;
+                const int64_t v2 = t2 ? lv : iv;
+                lf = t2 ? lf2 - 1 : lf2;
+                ih = t2 ? ih2 : ih2 + 1;
+                parent[c1] = a;
+                bit[c1] = 0;
+                parent[c2] = a;
+                bit[c2] = 1;
+                const int64_t sum = v1 + v2;
                 icount[a] = sum;
                 ring[a % kRing] = sum;
                 ++a;

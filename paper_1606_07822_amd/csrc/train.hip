@@ -2,24 +2,31 @@
 //
 // Worker = one wavefront. Wavefronts claim whole documents from a queue and
 // walk their kept centre words in order. Per centre v with window words
-// w_1..w_P the path of v is walked once: each inner-node row is loaded once,
-// updated by every window word in order (dot, sigmoid, gradient, two axpys)
-// and its change written back once; the hidden-layer gradients of the window
-// words stay in registers and are added to syn0 after the path. Swapping the
-// window and node loops of Algorithm 1 this way is the same computation
-// whenever a window holds no repeated word.
+// w_1..w_P the path of v is walked once, four inner nodes at a time: the
+// four rows are loaded together (the next four are prefetched), every window
+// word in order updates all four (dot, sigmoid, gradient, two axpys), and the
+// change of each row is written back once. The hidden-layer gradients of the
+// window words stay in registers and are added to syn0 after the path.
+// Swapping the window and node loops of Algorithm 1 this way is the same
+// computation whenever a window holds no repeated word; the four nodes of a
+// chunk never interact (a path visits distinct nodes).
+//
+// Cross-lane work of one window word and a chunk: the four dot products are
+// reduced together (two permlane32 swaps, one permlane16 swap, four DPP adds),
+// leaving node j's value in the 16 lanes of row j; the sigmoid and gradient
+// are then evaluated for the four nodes at once.
 //
 // Cache (§3.2): the cache owner is the workgroup. The rows of the top
 // cache_k inner nodes (the k created last by the Huffman merge) sit in LDS as
 // `val` (current) and `orig` (value at the last write-back); waves update
 // `val` with LDS atomic adds of their change. Every flush_every centres of the
-// workgroup, one wave writes val - orig back to HBM with an atomic add and
-// re-bases both copies on the returned HBM value (the write-back plus the
-// refill of Algorithm 1's flush, without stopping the other waves).
+// workgroup, one wave writes flush_scale * (val - orig) back to HBM with an
+// atomic add and re-bases both copies on the returned HBM value (write-back
+// plus refill, without stopping the other waves).
 //
 // Rows are spread over the 64 lanes element-strided: lane l holds elements
-// l, l+64, l+128, ... so every row load is a run of coalesced 256-byte
-// accesses and every dot product ends in one cross-lane reduction.
+// l, l+64, l+128, ... so every row access is a run of coalesced 256-byte
+// accesses.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -27,22 +34,53 @@
 #include "w2v_internal.h"
 
 namespace w2v {
-
-
 namespace {
 
-constexpr int kWavesPerBlock = 8;
-constexpr int kBlock = kWavesPerBlock * kWave;
+constexpr int kChunk = 4;            // inner nodes per step (one per 16-lane row)
+constexpr int kMinDocsPerWave = 8;   // automatic launch size: documents per wavefront, at least
 
-__device__ __forceinline__ float sigmoid_fast(float z) {
-    return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
-}
+__device__ __forceinline__ float sigmoid_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 __device__ __forceinline__ void lds_add(float *p, float v) { atomicAdd(p, v); }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over the 16 lanes of each row, result in every lane of the row.
+__device__ __forceinline__ float row_sum(float v) {
+    v += dpp<0xB1>(v);    // quad_perm [1,0,3,2]
+    v += dpp<0x4E>(v);    // quad_perm [2,3,0,1]
+    v += dpp<0x141>(v);   // row_half_mirror
+    v += dpp<0x140>(v);   // row_mirror
+    return v;
+}
+
+// Swap the upper 32 lanes of a with the lower 32 lanes of b (permlane32), or the
+// odd rows of a with the even rows of b (permlane16). Issued as inline assembly:
+// the compiler's builtins for these swaps fold the second result into the first
+// when both are consumed by one expression. The s_nop pairs cover the VALU
+// write-to-read distance the swaps need.
+__device__ __forceinline__ void swap32(float &a, float &b) {
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void swap16(float &a, float &b) {
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+
+// Four per-lane partial sums -> one register whose row j (lanes 16j..16j+15)
+// holds the full 64-lane sum of a_j.
+__device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3) {
+    swap32(a0, a2);
+    float r = a0 + a2;   // lanes 0-31: a0, lanes 32-63: a2 (each summed over lane pairs l, l+32)
+    swap32(a1, a3);
+    float q = a1 + a3;   // lanes 0-31: a1, lanes 32-63: a3
+    swap16(r, q);
+    return row_sum(r + q);   // rows: a0 a1 a2 a3
+}
+
 // One wave writes the cache's change back to HBM and re-bases val/orig on the result.
-// flush_scale = 1 adds the change as in the paper; < 1 adds a fraction of it (the
-// workgroups' local progress on the cached rows is then averaged rather than summed).
 __device__ void flush_cache_wave(const TrainArgs &a, float *val, float *orig, int lane) {
     for (int s = 0; s < a.cache_k; ++s) {
         float *g = a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride;
@@ -71,6 +109,12 @@ __device__ __forceinline__ void load_row(float (&r)[NE], const float *__restrict
 }
 
 template <int NE>
+__device__ __forceinline__ void zero_row(float (&r)[NE]) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i) r[i] = 0.0f;
+}
+
+template <int NE>
 __device__ __forceinline__ float dot_partial(const float (&x)[NE], const float (&y)[NE]) {
     float s = 0.0f;
 #pragma unroll
@@ -78,9 +122,102 @@ __device__ __forceinline__ float dot_partial(const float (&x)[NE], const float (
     return s;
 }
 
-// ARCH 0: skip-gram; ARCH 1: CBOW. PMAX >= 2 * window.
-template <int NE, int PMAX, int ARCH>
-__global__ __launch_bounds__(kBlock) void k_train(TrainArgs a) {
+// Rows of nodes c0 .. c0+3 of the path (zeros past its end), from LDS when cached.
+template <int NE>
+__device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainArgs &a, const float *val, int my_pt,
+                                           int c0, int len, int lane) {
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+        if (c0 + j < len) {
+            const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
+            if (n >= a.cache_first) load_row<NE>(y[j], val + (n - a.cache_first) * a.dim, lane, a.dim);
+            else load_row<NE>(y[j], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
+        } else {
+            zero_row<NE>(y[j]);
+        }
+    }
+}
+
+// Walk the path of the centre with the inputs x[0..nx) (in order), accumulating
+// the hidden-layer gradients into e[0..nx). PG = compile-time bound of nx.
+template <int NE, int PG, bool PREFETCH>
+__device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const float (&x)[PG][NE],
+                                          float (&e)[PG][NE], int nx, int my_pt, int len, uint64_t code, float alpha,
+                                          int lane) {
+    float yc[kChunk][NE], yn[kChunk][NE], y0[kChunk][NE];
+    load_chunk<NE>(yc, a, val, my_pt, 0, len, lane);
+    const int row = lane >> 4;
+    for (int c0 = 0; c0 < len; c0 += kChunk) {
+        if (PREFETCH && c0 + kChunk < len) load_chunk<NE>(yn, a, val, my_pt, c0 + kChunk, len, lane);
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+            for (int i = 0; i < NE; ++i) y0[j][i] = yc[j][i];
+        const int bitpos = c0 + row;
+        const float t = (bitpos < 64) ? static_cast<float>((code >> bitpos) & 1ull) : 0.0f;
+        const float one_minus_t = 1.0f - t;
+        const int nc = min(kChunk, len - c0);
+#pragma unroll
+        for (int p = 0; p < PG; ++p) {
+            if (p < nx) {
+                const float z = reduce4(dot_partial<NE>(x[p], yc[0]), dot_partial<NE>(x[p], yc[1]),
+                                        dot_partial<NE>(x[p], yc[2]), dot_partial<NE>(x[p], yc[3]));
+                const float gr = (one_minus_t - sigmoid_fast(z)) * alpha;
+#pragma unroll
+                for (int j = 0; j < kChunk; ++j) {
+                    if (j < nc) {
+                        const float gj =
+                            __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gr), 16 * j));
+#pragma unroll
+                        for (int i = 0; i < NE; ++i) {
+                            e[p][i] = fmaf(gj, yc[j][i], e[p][i]);
+                            yc[j][i] = fmaf(gj, x[p][i], yc[j][i]);
+                        }
+                    }
+                }
+            }
+        }
+        // write the change of each row back once
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j) {
+            if (j < nc) {
+                const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
+                if (n >= a.cache_first) {
+                    float *lrow = val + (n - a.cache_first) * a.dim;
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) {
+                        const int col = lane + i * kWave;
+                        if (col < a.dim) lds_add(lrow + col, yc[j][i] - y0[j][i]);
+                    }
+                } else {
+                    float *grow = a.syn1 + static_cast<int64_t>(n) * a.stride;
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) {
+                        const int col = lane + i * kWave;
+                        if (col < a.dim) {
+                            if (a.write_policy & 1) grow[col] = yc[j][i];
+                            else atomicAdd(grow + col, yc[j][i] - y0[j][i]);
+                        }
+                    }
+                }
+            }
+        }
+        if (c0 + kChunk < len) {
+            if (PREFETCH) {
+#pragma unroll
+                for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) yc[j][i] = yn[j][i];
+            } else {
+                load_chunk<NE>(yc, a, val, my_pt, c0 + kChunk, len, lane);
+            }
+        }
+    }
+}
+
+// ARCH 0: skip-gram, window words in groups of PG; ARCH 1: CBOW (one input, the mean).
+template <int NE, int PG, int ARCH, int WPB, bool PREFETCH>
+__global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     extern __shared__ float lds[];
     float *val = lds;
     float *orig = lds + a.cache_k * a.dim;
@@ -100,7 +237,7 @@ __global__ __launch_bounds__(kBlock) void k_train(TrainArgs a) {
     }
     __syncthreads();
 
-    const int gw = blockIdx.x * kWavesPerBlock + static_cast<int>(threadIdx.x / kWave);
+    const int gw = blockIdx.x * WPB + static_cast<int>(threadIdx.x / kWave);
     uint64_t n_kept = 0, n_pairs = 0, n_nodes = 0;
     if (gw < a.workers) {
         while (true) {
@@ -133,108 +270,64 @@ __global__ __launch_bounds__(kBlock) void k_train(TrainArgs a) {
                     const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
 
                     if constexpr (ARCH == 0) {
-                        float x[PMAX][NE], e[PMAX][NE];
+                        // groups of PG window words walk the path in turn (one group when P <= PG)
+                        for (int g0 = 0; g0 < P; g0 += PG) {
+                            const int nx = min(PG, P - g0);
+                            float x[PG][NE], e[PG][NE];
 #pragma unroll
-                        for (int p = 0; p < PMAX; ++p) {
-                            if (p < P) {
-                                const int w = __builtin_amdgcn_readlane(wv, p);
-                                load_row<NE>(x[p], a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
+                            for (int p = 0; p < PG; ++p) {
+                                if (p < nx) {
+                                    const int w = __builtin_amdgcn_readlane(wv, g0 + p);
+                                    load_row<NE>(x[p], a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
+                                } else {
+                                    zero_row<NE>(x[p]);
+                                }
+                                zero_row<NE>(e[p]);
                             }
+                            walk_path<NE, PG, PREFETCH>(a, val, x, e, nx, my_pt, len, code, alpha, lane);
 #pragma unroll
-                            for (int i = 0; i < NE; ++i) e[p][i] = 0.0f;
-                        }
-                        for (int jn = 0; jn < len; ++jn) {
-                            const int n = __builtin_amdgcn_readlane(my_pt, jn);
-                            const float t = static_cast<float>((code >> jn) & 1ull);
-                            const bool cached = n >= a.cache_first;
-                            float *lrow = val + (n - a.cache_first) * a.dim;
-                            float *grow = a.syn1 + static_cast<int64_t>(n) * a.stride;
-                            float y[NE], y0[NE];
-                            if (cached) load_row<NE>(y, lrow, lane, a.dim);
-                            else load_row<NE>(y, grow, lane, a.dim);
-#pragma unroll
-                            for (int i = 0; i < NE; ++i) y0[i] = y[i];
-#pragma unroll
-                            for (int p = 0; p < PMAX; ++p) {
-                                if (p < P) {
-                                    const float z = wave_sum(dot_partial<NE>(x[p], y));
-                                    const float f = sigmoid_fast(z);
-                                    const float gr = (1.0f - t - f) * alpha;
+                            for (int p = 0; p < PG; ++p) {
+                                if (p < nx) {
+                                    const int w = __builtin_amdgcn_readlane(wv, g0 + p);
+                                    float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
 #pragma unroll
                                     for (int i = 0; i < NE; ++i) {
-                                        e[p][i] = fmaf(gr, y[i], e[p][i]);
-                                        y[i] = fmaf(gr, x[p][i], y[i]);
+                                        const int col = lane + i * kWave;
+                                        if (col < a.dim) {
+                                            if (a.write_policy & 2) xr[col] = x[p][i] + e[p][i];
+                                            else atomicAdd(xr + col, e[p][i]);
+                                        }
                                     }
-                                }
-                            }
-#pragma unroll
-                            for (int i = 0; i < NE; ++i) {
-                                const int col = lane + i * kWave;
-                                if (col < a.dim) {
-                                    if (cached) lds_add(lrow + col, y[i] - y0[i]);
-                                    else if (a.write_policy == 0) atomicAdd(grow + col, y[i] - y0[i]);
-                                    else grow[col] = y[i];
-                                }
-                            }
-                        }
-#pragma unroll
-                        for (int p = 0; p < PMAX; ++p) {
-                            if (p < P) {
-                                const int w = __builtin_amdgcn_readlane(wv, p);
-                                float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
-#pragma unroll
-                                for (int i = 0; i < NE; ++i) {
-                                    const int col = lane + i * kWave;
-                                    if (col < a.dim) atomicAdd(xr + col, e[p][i]);
                                 }
                             }
                         }
                         n_nodes += static_cast<uint64_t>(P) * len;
                     } else {
                         // CBOW: h = mean of the window vectors; one path walk; e added to each window vector
-                        float h[NE], e[NE];
-#pragma unroll
-                        for (int i = 0; i < NE; ++i) { h[i] = 0.0f; e[i] = 0.0f; }
+                        float h[1][NE], e[1][NE];
+                        zero_row<NE>(h[0]);
+                        zero_row<NE>(e[0]);
                         for (int p = 0; p < P; ++p) {
                             const int w = __builtin_amdgcn_readlane(wv, p);
                             float xr[NE];
                             load_row<NE>(xr, a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
 #pragma unroll
-                            for (int i = 0; i < NE; ++i) h[i] += xr[i];
+                            for (int i = 0; i < NE; ++i) h[0][i] += xr[i];
                         }
                         const float fP = static_cast<float>(P);
 #pragma unroll
-                        for (int i = 0; i < NE; ++i) h[i] = h[i] / fP;
-                        for (int jn = 0; jn < len; ++jn) {
-                            const int n = __builtin_amdgcn_readlane(my_pt, jn);
-                            const float t = static_cast<float>((code >> jn) & 1ull);
-                            const bool cached = n >= a.cache_first;
-                            float *lrow = val + (n - a.cache_first) * a.dim;
-                            float *grow = a.syn1 + static_cast<int64_t>(n) * a.stride;
-                            float y[NE];
-                            if (cached) load_row<NE>(y, lrow, lane, a.dim);
-                            else load_row<NE>(y, grow, lane, a.dim);
-                            const float z = wave_sum(dot_partial<NE>(h, y));
-                            const float gr = (1.0f - t - sigmoid_fast(z)) * alpha;
-#pragma unroll
-                            for (int i = 0; i < NE; ++i) {
-                                const int col = lane + i * kWave;
-                                e[i] = fmaf(gr, y[i], e[i]);
-                                const float d = gr * h[i];
-                                if (col < a.dim) {
-                                    if (cached) lds_add(lrow + col, d);
-                                    else if (a.write_policy == 0) atomicAdd(grow + col, d);
-                                    else grow[col] = y[i] + d;
-                                }
-                            }
-                        }
+                        for (int i = 0; i < NE; ++i) h[0][i] = h[0][i] / fP;
+                        walk_path<NE, 1, PREFETCH>(a, val, h, e, 1, my_pt, len, code, alpha, lane);
                         for (int p = 0; p < P; ++p) {
                             const int w = __builtin_amdgcn_readlane(wv, p);
                             float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
 #pragma unroll
                             for (int i = 0; i < NE; ++i) {
                                 const int col = lane + i * kWave;
-                                if (col < a.dim) atomicAdd(xr + col, e[i]);
+                                if (col < a.dim) {
+                                    if (a.write_policy & 2) xr[col] = xr[col] + e[0][i];
+                                    else atomicAdd(xr + col, e[0][i]);
+                                }
                             }
                         }
                         n_nodes += len;
@@ -273,29 +366,28 @@ __global__ __launch_bounds__(kBlock) void k_train(TrainArgs a) {
     }
 }
 
-using TrainFn = void (*)(TrainArgs);
+struct Variant {
+    void (*fn)(TrainArgs);
+    int waves_per_block;
+};
 
-template <int NE, int ARCH>
-TrainFn pick_pmax(int pmax) {
-    if constexpr (ARCH == 1) {
-        (void)pmax;
-        return k_train<NE, 2, 1>;
-    } else {
-        if (pmax <= 4) return k_train<NE, 4, ARCH>;
-        if (pmax <= 10) return k_train<NE, 10, ARCH>;
-        return k_train<NE, 20, ARCH>;
-    }
+template <int NE, int PG, int WPB, bool PF>
+Variant variant(int arch) {
+    if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB};
+    return Variant{k_train<NE, 1, 1, WPB, PF>, WPB};
 }
 
-template <int ARCH>
-TrainFn pick_ne(int dim, int pmax) {
+// Register budget per lane: x and e take 2*PG*NE, the chunk rows 2 (3 with the
+// prefetch) * 4 * NE. Occupancy beats prefetch: at dim 300, 3 waves per SIMD
+// without the prefetch ran 21 % faster than 2 with it.
+Variant pick_variant(int arch, int dim) {
     const int ne = (dim + kWave - 1) / kWave;
-    if (ne <= 1) return pick_pmax<1, ARCH>(pmax);
-    if (ne <= 2) return pick_pmax<2, ARCH>(pmax);
-    if (ne <= 4) return pick_pmax<4, ARCH>(pmax);
-    if (ne <= 5) return pick_pmax<5, ARCH>(pmax);
-    if (ne <= 8) return pick_pmax<8, ARCH>(pmax);
-    return pick_pmax<16, ARCH>(pmax);
+    if (ne <= 1) return variant<1, 20, 16, true>(arch);
+    if (ne <= 2) return variant<2, 20, 12, true>(arch);
+    if (ne <= 4) return variant<4, 10, 12, true>(arch);
+    if (ne <= 5) return variant<5, 10, 12, false>(arch);
+    if (ne <= 8) return variant<8, 4, 8, false>(arch);
+    return variant<16, 2, 8, false>(arch);
 }
 
 __global__ void k_zero_train(int32_t *queue, unsigned long long *stats) {
@@ -319,27 +411,33 @@ size_t train_lds_bytes(int32_t cache_k, int32_t dim) { return 2ull * cache_k * d
 
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals) {
+    (void)window;
     const size_t lds = train_lds_bytes(a.cache_k, a.dim);
-    TrainFn fn = arch == 0 ? pick_ne<0>(a.dim, 2 * window) : pick_ne<1>(a.dim, 2 * window);
+    const Variant v = pick_variant(arch, a.dim);
+    const int block = v.waves_per_block * kWave;
     if (lds > 64 * 1024)
-        W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
+        W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(v.fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(lds)));
     int grid;
     if (a.workers > 0) {
-        grid = static_cast<int>(ceil_div(a.workers, kWavesPerBlock));
+        grid = static_cast<int>(ceil_div(a.workers, v.waves_per_block));
     } else {
         int per_cu = 0;
-        W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn), kBlock,
+        W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(v.fn), block,
                                                              lds));
         grid = device_cu_count() * std::max(1, per_cu);
-        a.workers = grid * kWavesPerBlock;
+        // every wavefront gets at least kMinDocsPerWave documents, so that every workgroup
+        // (cache owner) contributes to the averaged write-back of the cached rows
+        const int64_t by_docs = ceil_div(a.n_docs, static_cast<int64_t>(v.waves_per_block) * kMinDocsPerWave);
+        grid = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(grid, by_docs)));
+        a.workers = grid * v.waves_per_block;
     }
     if (a.flush_scale <= 0.0f) a.flush_scale = 1.0f / static_cast<float>(grid);
     record_train_launch(grid, a.workers);
     k_zero_train<<<1, 64, 0, s>>>(a.queue, a.stats);
     W2V_LAUNCH_CHECK("k_zero_train");
     if (ev0) W2V_HIP(hipEventRecord(ev0, s));
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(kBlock), lds, s, a);
+    hipLaunchKernelGGL(v.fn, dim3(grid), dim3(block), lds, s, a);
     W2V_LAUNCH_CHECK("k_train");
     if (ev1) W2V_HIP(hipEventRecord(ev1, s));
     if (stats_out) {

@@ -292,8 +292,8 @@ def async_ll(w2v, s, held, **kw):
     return sg / npairs, npairs
 
 
-@pytest.mark.parametrize("kw", [dict(cache_k=0), dict(cache_k=31, flush_every=10, flush_policy=0),
-                                dict(cache_k=31)])
+@pytest.mark.parametrize("kw", [dict(cache_k=0), dict(cache_k=31, flush_every=10, flush_policy=0, write_policy=0),
+                                dict(cache_k=31), dict(cache_k=31, write_policy=0)])
 def test_async_loglik_within_1pct_tiny(w2v, kw):
     s = oracle_side("tiny_sg_v1k_d50")
     held = corpus("tiny_sg_v1k_d50", heldout=True)
@@ -317,13 +317,16 @@ def golden(name):
 
 
 # Default asynchronous mode (top-31 cache in LDS, write-back of the workgroups' averaged change every
-# 1000 centres, atomic adds elsewhere) at full occupancy; the uncached Hogwild store policy; and the
-# cache with the paper's summed write-back, which is stable only at low concurrency (256 wavefronts).
+# 1000 centres, Hogwild row stores elsewhere) at full occupancy; the same with atomic adds of the change
+# for uncached rows; no cache; and the cache with the paper's summed write-back, which is stable only
+# at low concurrency (256 wavefronts).
 @pytest.mark.parametrize("name,kw", [
     ("sg_v30k_d100", {}),
-    ("sg_v30k_d100", dict(cache_k=0, write_policy=1)),
-    ("sg_v30k_d100", dict(workers=256, cache_k=31, flush_every=10, flush_policy=0)),
+    ("sg_v30k_d100", dict(write_policy=0)),
+    ("sg_v30k_d100", dict(cache_k=0)),
+    ("sg_v30k_d100", dict(workers=256, cache_k=31, flush_every=10, flush_policy=0, write_policy=0)),
     ("sg_v100k_d200", {}),
+    ("sg_v100k_d200", dict(write_policy=0)),
     ("cbow_v100k_d300", {}),
 ])
 def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw):
