@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--write-policy", type=int, default=1)
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 1 GiB device-to-device copy first (reference dispatch for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -115,6 +117,13 @@ def main():
     held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
     ws = torch.empty(w2v.train_workspace_bytes(model, w.n_tokens, p), dtype=torch.uint8, device=dev)
     stats = torch.zeros(w2v.N_STATS, dtype=torch.int64, device=dev)
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # byte model of one launch (the sampler's keep mask with the training seed)
     pr = w2v.sample_pairs(voc.tokens, voc.V, voc.vocab_counts, voc.train_words, p, cap=0, want_mask=True)

@@ -3,10 +3,10 @@
 // Construction rule: leaves in ascending count (vocabulary index V-1 first),
 // inner nodes in creation order; each merge takes the smaller front twice, a
 // leaf winning a count tie; the first child taken gets bit 0; merge a creates
-// inner node a (root = V-2). The merge is an inherently sequential chain; one
-// lane runs it out of LDS (leaf counts and old inner counts are staged in
-// chunks by the whole wave, recent inner counts sit in a ring), then parallel
-// kernels derive codes, offsets and points.
+// inner node a (root = V-2). The merge is a sequential chain except where it
+// runs through many equal-kind merges in a row (the tail of a skewed
+// vocabulary); those runs are written by the whole block, the rest by one lane.
+// Parallel kernels then derive codes, offsets and points.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -16,88 +16,132 @@
 namespace w2v {
 namespace {
 
-constexpr int kChunk = 1024;   // leaf / inner counts staged per refill
-constexpr int kRing = 4096;    // most recent inner counts
+constexpr int kMergeThreads = 256;
+constexpr int kRunMin = 32;   // runs of at least this many merges are written by the whole block
 
-__global__ __launch_bounds__(64) void k_huff_merge(const int64_t *__restrict__ leaf_count, int32_t V,
-                                                   int32_t *__restrict__ parent, uint8_t *__restrict__ bit,
-                                                   int64_t *__restrict__ icount) {
-    __shared__ int64_t lstage[kChunk];   // lstage[i] = count of leaf (l_hi - i)
-    __shared__ int64_t istage[kChunk];   // istage[i] = icount[i_lo + i], i < i_n
-    __shared__ int64_t ring[kRing];      // ring[a % kRing] = icount[a] for the last kRing merges
-    __shared__ int32_t st[6];            // lf, ih, a, l_hi, i_lo, i_n
-    __shared__ int32_t need;             // 1 = leaves, 2 = inner counts
-    const int lane = threadIdx.x;
-    if (lane == 0) {
-        st[0] = V - 1; st[1] = 0; st[2] = 0; st[3] = -1; st[4] = 0; st[5] = 0;
-        need = 1;
+// Leaves in ascending count: position p is vocabulary index V-1-p.
+__device__ __forceinline__ int64_t leaf_val(const int64_t *__restrict__ counts, int32_t V, int32_t p) {
+    return counts[V - 1 - p];
+}
+
+// Two-queue merge, written in phases. While the next merges alternate between the
+// queues, lane 0 performs them one by one. When the next >= kRunMin merges all take
+// two leaves (every leaf up to the 2m-th is <= the inner front, which those merges
+// leave in place) or all take two inner nodes (every one of the next 2m inner nodes
+// is < the leaf front), the block writes the whole run at once: merge a+i takes
+// elements 2i (bit 0) and 2i+1 (bit 1) of that queue. New inner nodes join the back
+// of their queue and never take part in the run that creates them.
+__global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__restrict__ counts, int32_t V,
+                                                              int32_t *__restrict__ parent, uint8_t *__restrict__ bit,
+                                                              int64_t *__restrict__ icount, int32_t *__restrict__ flags) {
+    __shared__ int32_t s_pl, s_ih, s_a, s_mode, s_m;
+    __shared__ int64_t s_front;
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        s_pl = 0;
+        s_ih = 0;
+        s_a = 0;
     }
     __syncthreads();
-    while (true) {
-        const int32_t nd = need;
-        if (nd == 1) {
-            const int32_t hi = st[0];
-            for (int i = lane; i < kChunk; i += 64) lstage[i] = (hi - i >= 0) ? leaf_count[hi - i] : 0;
-            __syncthreads();
-            if (lane == 0) st[3] = hi;
-        } else if (nd == 2) {
-            const int32_t lo = st[1], a = st[2];
-            const int32_t n = min(kChunk, a - lo);
-            for (int i = lane; i < n; i += 64) istage[i] = icount[lo + i];
-            __syncthreads();
-            if (lane == 0) { st[4] = lo; st[5] = n; }
-        }
-        __syncthreads();
-        if (lane == 0) {
-            int32_t lf = st[0], ih = st[1], a = st[2];
-            const int32_t l_hi = st[3], i_lo = st[4], i_n = st[5];
-            int32_t want = 0;
-            // leaf idx is readable iff staged; inner idx (< a) iff in the ring or the stage
-            auto leaf_ok = [&](int32_t idx) { return idx < 0 || (idx <= l_hi && idx > l_hi - kChunk); };
-            auto inner_ok = [&](int32_t idx, int32_t aa) {
-                return idx >= aa || aa - idx <= kRing || (idx >= i_lo && idx < i_lo + i_n);
-            };
-            auto leaf_at = [&](int32_t idx) { return lstage[l_hi - idx]; };
-            auto inner_at = [&](int32_t idx, int32_t aa) {
-                return (aa - idx <= kRing) ? ring[idx % kRing] : istage[idx - i_lo];
-            };
+    const int64_t max_phases = 4LL * V + 16;   // every phase merges at least once
+    for (int64_t phase = 0; phase < max_phases; ++phase) {
+        if (tid == 0) {
+            int32_t pl = s_pl, ih = s_ih, a = s_a;
+            int mode = 0;   // 0 done, 1 leaf run, 2 inner run
+            int64_t front = 0;
             while (a < V - 1) {
-                if (!leaf_ok(lf) || !leaf_ok(lf - 1)) { want = 1; break; }
-                if (!inner_ok(ih, a) || !inner_ok(ih + 1, a)) { want = 2; break; }
-                // the two fronts of each queue, read together
-                const int64_t L0 = lf >= 0 ? leaf_at(lf) : 0;
-                const int64_t L1 = lf >= 1 ? leaf_at(lf - 1) : 0;
-                const int64_t I0 = ih < a ? inner_at(ih, a) : 0;
-                const int64_t I1 = ih + 1 < a ? inner_at(ih + 1, a) : 0;
-                // first child (bit 0): a leaf wins a tie
-                const bool t1 = lf >= 0 && (ih >= a || L0 <= I0);
-                const int32_t c1 = t1 ? lf : V + ih;
-                const int64_t v1 = t1 ? L0 : I0;
-                const int32_t lf2 = t1 ? lf - 1 : lf, ih2 = t1 ? ih : ih + 1;
-                const int64_t lv = t1 ? L1 : L0, iv = t1 ? I0 : I1;
-                // second child (bit 1)
-                const bool t2 = lf2 >= 0 && (ih2 >= a || lv <= iv);
-                const int32_t c2 = t2 ? lf2 : V + ih2;
-                const int64_t v2 = t2 ? lv : iv;
-                lf = t2 ? lf2 - 1 : lf2;
-                ih = t2 ? ih2 : ih2 + 1;
-                parent[c1] = a;
-                bit[c1] = 0;
-                parent[c2] = a;
-                bit[c2] = 1;
-                const int64_t sum = v1 + v2;
+                const int32_t nl = V - pl, ni = a - ih;
+                const int64_t FI = ni > 0 ? icount[ih] : 0;
+                const int64_t FL = nl > 0 ? leaf_val(counts, V, pl) : 0;
+                if (ni > 0 && nl >= 2 * kRunMin && leaf_val(counts, V, pl + 2 * kRunMin - 1) <= FI) {
+                    mode = 1;
+                    front = FI;
+                    break;
+                }
+                if (ni >= 2 * kRunMin && (nl == 0 || icount[ih + 2 * kRunMin - 1] < FL)) {
+                    mode = 2;
+                    front = nl > 0 ? FL : INT64_MAX;
+                    break;
+                }
+                // one merge: a leaf wins a tie
+                int64_t sum = 0;
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const bool use_leaf = pl < V && (ih >= a || leaf_val(counts, V, pl) <= icount[ih]);
+                    int32_t child;
+                    if (use_leaf) {
+                        sum += leaf_val(counts, V, pl);
+                        child = V - 1 - pl;
+                        ++pl;
+                    } else {
+                        sum += icount[ih];
+                        child = V + ih;
+                        ++ih;
+                    }
+                    parent[child] = a;
+                    bit[child] = static_cast<uint8_t>(b);
+                }
                 icount[a] = sum;
-                ring[a % kRing] = sum;
                 ++a;
             }
-            st[0] = lf; st[1] = ih; st[2] = a;
-            need = want;
-            // make this lane's global icount stores visible to the wave before a stage refill
+            s_pl = pl;
+            s_ih = ih;
+            s_a = a;
+            s_mode = mode;
+            s_front = front;
             __threadfence_block();
         }
         __syncthreads();
-        if (need == 0) break;
+        const int mode = s_mode;
+        if (mode == 0) return;
+        const int32_t pl = s_pl, ih = s_ih, a = s_a;
+        const int64_t front = s_front;
+        // length of the run: the queue's elements below the other front form a prefix
+        int32_t n = 0;
+        const int32_t avail = mode == 1 ? V - pl : a - ih;
+        for (int32_t off = 0; off < avail; off += kMergeThreads) {
+            const int32_t q = off + tid;
+            bool ok = false;
+            if (q < avail) ok = mode == 1 ? leaf_val(counts, V, pl + q) <= front : icount[ih + q] < front;
+            const int c = __syncthreads_count(ok);
+            n += c;
+            if (c < kMergeThreads) break;
+        }
+        const int32_t m = n / 2;
+        if (m == 0) {   // impossible for descending counts (the probe saw a run of kRunMin)
+            if (tid == 0) atomicOr(&flags[2], 1);
+            return;
+        }
+        for (int32_t i = tid; i < m; i += kMergeThreads) {
+            int32_t c0, c1;
+            int64_t v0, v1;
+            if (mode == 1) {
+                c0 = V - 1 - (pl + 2 * i);
+                c1 = c0 - 1;
+                v0 = leaf_val(counts, V, pl + 2 * i);
+                v1 = leaf_val(counts, V, pl + 2 * i + 1);
+            } else {
+                c0 = V + ih + 2 * i;
+                c1 = c0 + 1;
+                v0 = icount[ih + 2 * i];
+                v1 = icount[ih + 2 * i + 1];
+            }
+            parent[c0] = a + i;
+            bit[c0] = 0;
+            parent[c1] = a + i;
+            bit[c1] = 1;
+            icount[a + i] = v0 + v1;
+        }
+        __threadfence_block();
+        __syncthreads();
+        if (tid == 0) {
+            if (mode == 1) s_pl = pl + 2 * m;
+            else s_ih = ih + 2 * m;
+            s_a = a + m;
+        }
+        __syncthreads();
     }
+    if (tid == 0) atomicOr(&flags[2], 1);   // phase cap reached: malformed counts
 }
 
 // codelen / code per leaf; maxlen and error flag (code longer than 64).
@@ -208,17 +252,18 @@ int run_build_huffman(const int64_t *vocab_counts, int32_t V, uint8_t *codelen, 
     const unsigned gv = static_cast<unsigned>(ceil_div(V, 256));
     k_zero_i32<<<1, 64, 0, s>>>(flags, 4);
     k_fill_parent<<<static_cast<unsigned>(ceil_div(2LL * V, 256)), 256, 0, s>>>(parent, 2 * V);
-    k_huff_merge<<<1, 64, 0, s>>>(vocab_counts, V, parent, bit, icount);
+    k_huff_merge<<<1, kMergeThreads, 0, s>>>(vocab_counts, V, parent, bit, icount, flags);
     W2V_LAUNCH_CHECK("k_huff_merge");
     k_huff_codes<<<gv, 256, 0, s>>>(parent, bit, V, codelen, code, flags);
     W2V_LAUNCH_CHECK("k_huff_codes");
     k_scan_codelen<<<1, kScanThreads, 0, s>>>(codelen, V, point_off, total);
     W2V_LAUNCH_CHECK("k_scan_codelen");
-    int32_t hflags[2];
+    int32_t hflags[3];
     int64_t htotal = 0;
     W2V_HIP(hipMemcpyAsync(hflags, flags, sizeof(hflags), hipMemcpyDeviceToHost, s));
     W2V_HIP(hipMemcpyAsync(&htotal, total, sizeof(htotal), hipMemcpyDeviceToHost, s));
     W2V_HIP(hipStreamSynchronize(s));
+    if (hflags[2]) return fail(W2V_E_ARG, "vocab_counts must be in descending order");
     if (hflags[1]) return fail(W2V_E_RANGE, "a Huffman code is longer than 64 bits");
     *points_len_host = htotal;
     *max_len_host = hflags[0];
