@@ -100,7 +100,8 @@ int w2v_build_huffman(const int64_t *vocab_counts, int32_t V, uint8_t *codelen, 
  * syn0 ("vector[w]" of Algorithm 1) is float[V][row_stride], syn1
  * ("weight[n]", the inner-node vectors) is float[V-1][row_stride]; only the
  * first dim floats of a row are used. row_stride >= dim, a multiple of 4;
- * both arrays 16-byte aligned.
+ * both arrays 16-byte aligned. Training may write zeros into a row's padding
+ * columns (dim .. row_stride-1); their contents are otherwise ignored.
  * ---------------------------------------------------------------------- */
 typedef struct {
     float *syn0;

@@ -80,12 +80,13 @@ __device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3)
     return row_sum(r + q);   // rows: a0 a1 a2 a3
 }
 
-// One wave writes the cache's change back to HBM and re-bases val/orig on the result.
-__device__ void flush_cache_wave(const TrainArgs &a, float *val, float *orig, int lane) {
+// One wave writes the cache's change back to HBM and re-bases val/orig on the
+// result. LDS rows are ls floats apart (ls >= dim, padding kept at zero).
+__device__ void flush_cache_wave(const TrainArgs &a, float *val, float *orig, int ls, int lane) {
     for (int s = 0; s < a.cache_k; ++s) {
         float *g = a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride;
-        float *vs = val + s * a.dim;
-        float *os = orig + s * a.dim;
+        float *vs = val + s * ls;
+        float *os = orig + s * ls;
         for (int col = lane; col < a.dim; col += kWave) {
             const float c = vs[col];
             const float d = (c - os[col]) * a.flush_scale;
@@ -99,12 +100,46 @@ __device__ void flush_cache_wave(const TrainArgs &a, float *val, float *orig, in
     }
 }
 
+// Global row -> registers; columns past dim read as zero.
 template <int NE>
 __device__ __forceinline__ void load_row(float (&r)[NE], const float *__restrict__ p, int lane, int dim) {
 #pragma unroll
     for (int i = 0; i < NE; ++i) {
         const int col = lane + i * kWave;
         r[i] = (col < dim) ? p[col] : 0.0f;
+    }
+}
+
+// LDS row with zero padding up to NE*64 columns.
+template <int NE>
+__device__ __forceinline__ void load_row_lds(float (&r)[NE], const float *p, int lane) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i) r[i] = p[lane + i * kWave];
+}
+
+// Row writes. With full rows (row_stride >= NE*64) all NE*64 columns are written
+// (the padding columns receive zeros / zero changes) and no lane is masked.
+template <int NE>
+__device__ __forceinline__ void store_row(float *p, const float (&r)[NE], int lane, int dim, bool full) {
+    if (full) {
+#pragma unroll
+        for (int i = 0; i < NE; ++i) p[lane + i * kWave] = r[i];
+    } else {
+#pragma unroll
+        for (int i = 0; i < NE; ++i)
+            if (lane + i * kWave < dim) p[lane + i * kWave] = r[i];
+    }
+}
+
+template <int NE>
+__device__ __forceinline__ void atomic_add_row(float *p, const float (&r)[NE], int lane, int dim, bool full) {
+    if (full) {
+#pragma unroll
+        for (int i = 0; i < NE; ++i) atomicAdd(p + lane + i * kWave, r[i]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < NE; ++i)
+            if (lane + i * kWave < dim) atomicAdd(p + lane + i * kWave, r[i]);
     }
 }
 
@@ -130,7 +165,7 @@ __device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainAr
     for (int j = 0; j < kChunk; ++j) {
         if (c0 + j < len) {
             const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-            if (n >= a.cache_first) load_row<NE>(y[j], val + (n - a.cache_first) * a.dim, lane, a.dim);
+            if (n >= a.cache_first) load_row_lds<NE>(y[j], val + (n - a.cache_first) * (NE * kWave), lane);
             else load_row<NE>(y[j], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
         } else {
             zero_row<NE>(y[j]);
@@ -166,8 +201,8 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
 #pragma unroll
                 for (int j = 0; j < kChunk; ++j) {
                     if (j < nc) {
-                        const float gj =
-                            __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gr), 16 * j));
+                        const float gj = __builtin_bit_cast(
+                            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gr), 16 * j));
 #pragma unroll
                         for (int i = 0; i < NE; ++i) {
                             e[p][i] = fmaf(gj, yc[j][i], e[p][i]);
@@ -182,23 +217,17 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
         for (int j = 0; j < kChunk; ++j) {
             if (j < nc) {
                 const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-                if (n >= a.cache_first) {
-                    float *lrow = val + (n - a.cache_first) * a.dim;
+                float d[NE];
 #pragma unroll
-                    for (int i = 0; i < NE; ++i) {
-                        const int col = lane + i * kWave;
-                        if (col < a.dim) lds_add(lrow + col, yc[j][i] - y0[j][i]);
-                    }
+                for (int i = 0; i < NE; ++i) d[i] = yc[j][i] - y0[j][i];
+                if (n >= a.cache_first) {
+                    float *lrow = val + (n - a.cache_first) * (NE * kWave);
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) lds_add(lrow + lane + i * kWave, d[i]);
                 } else {
                     float *grow = a.syn1 + static_cast<int64_t>(n) * a.stride;
-#pragma unroll
-                    for (int i = 0; i < NE; ++i) {
-                        const int col = lane + i * kWave;
-                        if (col < a.dim) {
-                            if (a.write_policy & 1) grow[col] = yc[j][i];
-                            else atomicAdd(grow + col, yc[j][i] - y0[j][i]);
-                        }
-                    }
+                    if (a.write_policy & 1) store_row<NE>(grow, yc[j], lane, a.dim, a.full_rows);
+                    else atomic_add_row<NE>(grow, d, lane, a.dim, a.full_rows);
                 }
             }
         }
@@ -218,9 +247,10 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
 // ARCH 0: skip-gram, window words in groups of PG; ARCH 1: CBOW (one input, the mean).
 template <int NE, int PG, int ARCH, int WPB, bool PREFETCH>
 __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
+    constexpr int LS = NE * kWave;   // LDS row stride (zero padding past dim)
     extern __shared__ float lds[];
     float *val = lds;
-    float *orig = lds + a.cache_k * a.dim;
+    float *orig = lds + a.cache_k * LS;
     __shared__ int s_centres;
     __shared__ int s_lock;
     const int lane = lane_id();
@@ -228,10 +258,10 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
         s_centres = 0;
         s_lock = 0;
     }
-    const int kd = a.cache_k * a.dim;
+    const int kd = a.cache_k * LS;
     for (int i = threadIdx.x; i < kd; i += blockDim.x) {
-        const int s = i / a.dim, col = i - s * a.dim;
-        const float v = a.syn1[static_cast<int64_t>(a.cache_first + s) * a.stride + col];
+        const int s = i / LS, col = i - s * LS;
+        const float v = col < a.dim ? a.syn1[static_cast<int64_t>(a.cache_first + s) * a.stride + col] : 0.0f;
         val[i] = v;
         orig[i] = v;
     }
@@ -290,13 +320,13 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                                 if (p < nx) {
                                     const int w = __builtin_amdgcn_readlane(wv, g0 + p);
                                     float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
+                                    if (a.write_policy & 2) {
+                                        float nx_[NE];
 #pragma unroll
-                                    for (int i = 0; i < NE; ++i) {
-                                        const int col = lane + i * kWave;
-                                        if (col < a.dim) {
-                                            if (a.write_policy & 2) xr[col] = x[p][i] + e[p][i];
-                                            else atomicAdd(xr + col, e[p][i]);
-                                        }
+                                        for (int i = 0; i < NE; ++i) nx_[i] = x[p][i] + e[p][i];
+                                        store_row<NE>(xr, nx_, lane, a.dim, a.full_rows);
+                                    } else {
+                                        atomic_add_row<NE>(xr, e[p], lane, a.dim, a.full_rows);
                                     }
                                 }
                             }
@@ -321,13 +351,14 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                         for (int p = 0; p < P; ++p) {
                             const int w = __builtin_amdgcn_readlane(wv, p);
                             float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
+                            if (a.write_policy & 2) {
+                                float cur[NE];
+                                load_row<NE>(cur, xr, lane, a.dim);
 #pragma unroll
-                            for (int i = 0; i < NE; ++i) {
-                                const int col = lane + i * kWave;
-                                if (col < a.dim) {
-                                    if (a.write_policy & 2) xr[col] = xr[col] + e[0][i];
-                                    else atomicAdd(xr + col, e[0][i]);
-                                }
+                                for (int i = 0; i < NE; ++i) cur[i] += e[0][i];
+                                store_row<NE>(xr, cur, lane, a.dim, a.full_rows);
+                            } else {
+                                atomic_add_row<NE>(xr, e[0], lane, a.dim, a.full_rows);
                             }
                         }
                         n_nodes += len;
@@ -342,7 +373,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     }
                     go = __builtin_amdgcn_readfirstlane(go);
                     if (go) {
-                        flush_cache_wave(a, val, orig, lane);
+                        flush_cache_wave(a, val, orig, LS, lane);
                         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
                         if (lane == 0) atomicExch(&s_lock, 0);
                     }
@@ -359,22 +390,21 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     // final write-back of the cache
     for (int i = threadIdx.x; i < kd; i += blockDim.x) {
         const float d = (val[i] - orig[i]) * a.flush_scale;
-        if (d != 0.0f) {
-            const int s = i / a.dim, col = i - s * a.dim;
-            atomicAdd(a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride + col, d);
-        }
+        const int s = i / LS, col = i - s * LS;
+        if (d != 0.0f && col < a.dim) atomicAdd(a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride + col, d);
     }
 }
 
 struct Variant {
     void (*fn)(TrainArgs);
     int waves_per_block;
+    int ne;
 };
 
 template <int NE, int PG, int WPB, bool PF>
 Variant variant(int arch) {
-    if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB};
-    return Variant{k_train<NE, 1, 1, WPB, PF>, WPB};
+    if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE};
+    return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE};
 }
 
 // Register budget per lane: x and e take 2*PG*NE, the chunk rows 2 (3 with the
@@ -407,14 +437,19 @@ __global__ void k_write_stats(const int64_t *totals, const unsigned long long *t
 
 }  // namespace
 
-size_t train_lds_bytes(int32_t cache_k, int32_t dim) { return 2ull * cache_k * dim * sizeof(float); }
+size_t train_lds_bytes(int32_t cache_k, int32_t dim) {
+    const int ne = (dim + kWave - 1) / kWave;
+    const int ne_v = ne <= 2 ? ne : (ne <= 4 ? 4 : (ne <= 5 ? 5 : (ne <= 8 ? 8 : 16)));
+    return 2ull * cache_k * ne_v * kWave * sizeof(float);
+}
 
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals) {
     (void)window;
-    const size_t lds = train_lds_bytes(a.cache_k, a.dim);
     const Variant v = pick_variant(arch, a.dim);
+    const size_t lds = 2ull * a.cache_k * v.ne * kWave * sizeof(float);
     const int block = v.waves_per_block * kWave;
+    a.full_rows = a.stride >= v.ne * kWave ? 1 : 0;
     if (lds > 64 * 1024)
         W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(v.fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(lds)));

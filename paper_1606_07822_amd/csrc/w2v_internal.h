@@ -155,6 +155,7 @@ struct TrainArgs {
     int32_t cache_k, cache_first, flush_every;
     int32_t workers;
     int32_t write_policy;
+    int32_t full_rows;       // row_stride covers the variant's NE*64 columns: whole-row writes
     float flush_scale;       // fraction of the cached rows' change written back (1 = all of it)
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, node updates
