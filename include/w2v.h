@@ -137,7 +137,10 @@ typedef struct {
                                 bit 1: the same for the word vectors syn0 */
     int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), 1 = add the
                                 change divided by the number of workgroups (their progress averaged) */
-    int32_t reserved2[6];
+    int32_t hot_k;           /* with write_policy bit 0: the hot_k inner nodes created just before the cached
+                                ones (on most paths, so the most contended rows) still take atomic adds of
+                                their change; >= 0 */
+    int32_t reserved2[5];
 } w2v_params;
 
 /* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,
@@ -171,7 +174,9 @@ typedef struct {
  * (to read the number of kept centres).
  * stats: int64[W2V_N_STATS] device buffer, overwritten (may be NULL).
  * Errors: W2V_E_ARG for a bad model/params (V < 2, dim not in 1..1024,
- * window not in 1..10, LDS budget 2 cache_k dim 4 bytes exceeded, ...).
+ * window not in 1..10, LDS budget exceeded: 2 cache_k rows of 4-byte floats,
+ * a row being dim rounded up to 64, 128, 256, 320 or 512 for dim <= 512 and
+ * dim above, ...).
  * ---------------------------------------------------------------------- */
 size_t w2v_train_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
 int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,

@@ -44,7 +44,7 @@ class CParams(ctypes.Structure):
                 ("alpha0", ctypes.c_float), ("epoch", I32), ("n_epochs", I32), ("reserved1", I32),
                 ("corpus_tokens", I64), ("first_raw_index", I64), ("seed", U64), ("cache_k", I32),
                 ("flush_every", I32), ("sync_batch", I32), ("workers", I32), ("write_policy", I32),
-                ("flush_policy", I32), ("reserved2", I32 * 6)]
+                ("flush_policy", I32), ("hot_k", I32), ("reserved2", I32 * 5)]
 
 
 assert ctypes.sizeof(CModel) == 80 and ctypes.sizeof(CParams) == 112
@@ -233,8 +233,16 @@ def make_model(syn0_init, syn1_init, vocab: Vocab, tree: Tree, device="cuda") ->
     return Model(syn0, syn1, dim, vocab.vocab_counts.contiguous(), vocab.train_words, tree)
 
 
+# CBOW applies one update per node and centre, so its row stores lose more of
+# the contended upper nodes' changes than skip-gram's; by default those rows
+# take atomic adds there.
+HOT_K_CBOW = 1024
+
+
 @dataclass
 class Params:
+    """Fields of w2v_params (include/w2v.h). hot_k=None picks 0 for skip-gram
+    and HOT_K_CBOW for CBOW."""
     window: int
     sample: float = 0.0
     alpha0: float = 0.025
@@ -252,13 +260,19 @@ class Params:
     workers: int = 0
     write_policy: int = 1
     flush_policy: int = 1
+    hot_k: int | None = None
     extra: dict = field(default_factory=dict)
 
     def c(self) -> CParams:
         return CParams(self.arch, self.mode, self.window, self.doc_len, float(self.sample), float(self.alpha0),
                        self.epoch, self.n_epochs, 0, self.corpus_tokens, self.first_raw_index, self.seed,
                        self.cache_k, self.flush_every, self.sync_batch, self.workers, self.write_policy,
-                       self.flush_policy)
+                       self.flush_policy, self.resolved_hot_k())
+
+    def resolved_hot_k(self) -> int:
+        if self.hot_k is not None:
+            return self.hot_k
+        return HOT_K_CBOW if self.arch == 1 else 0
 
 
 # ---------------------------------------------------------------- training

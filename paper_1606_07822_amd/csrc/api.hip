@@ -20,6 +20,8 @@ size_t pairs_workspace_bytes(int32_t V, int64_t n_tokens, int32_t doc_len);
 int run_sample_pairs(const int32_t *, int64_t, int32_t, const int64_t *, int64_t, const w2v_params *, int64_t *,
                      int64_t *, int64_t, uint8_t *, int64_t *, int64_t *, uint64_t *, void *, hipStream_t);
 size_t train_lds_bytes(int32_t cache_k, int32_t dim);
+int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_docs, int *grid, int *waves);
+int64_t train_egrad_floats(int arch, int dim, int stride, int window, int waves);
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals);
 size_t sync_extra_bytes(int32_t V, int32_t dim, int64_t n_docs);
@@ -117,6 +119,7 @@ int check_params(const w2v_params *p, bool training) {
         if (p->workers < 0) return fail(W2V_E_ARG, "workers must be >= 0");
         if (p->write_policy < 0 || p->write_policy > 3) return fail(W2V_E_ARG, "write_policy must be in 0..3");
         if (p->flush_policy != 0 && p->flush_policy != 1) return fail(W2V_E_ARG, "flush_policy must be 0 or 1");
+        if (p->hot_k < 0) return fail(W2V_E_ARG, "hot_k must be >= 0");
     }
     return W2V_OK;
 }
@@ -157,6 +160,16 @@ __global__ void k_zero_stats(unsigned long long *p) {
     if (threadIdx.x < 4) p[threadIdx.x] = 0;
 }
 
+// Parked hidden-layer gradients of the asynchronous kernel (skip-gram windows
+// wider than one register group): floats, 0 when none are needed.
+int64_t egrad_floats(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
+    if (p->mode != 0) return 0;
+    int grid = 0, waves = 0;
+    const int64_t n_docs = n_tokens > 0 ? ceil_div(n_tokens, static_cast<int64_t>(p->doc_len)) : 0;
+    if (train_launch_shape(p->arch, m->dim, p->cache_k, p->workers, n_docs, &grid, &waves)) return 0;
+    return train_egrad_floats(p->arch, m->dim, m->row_stride, p->window, waves);
+}
+
 size_t train_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
     Carve c;
     sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
@@ -164,6 +177,7 @@ size_t train_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
     c.take<float>(static_cast<size_t>(span / 10000 + 3));   // alpha blocks
     c.take<int32_t>(4);                                     // queue
     c.take<unsigned long long>(4);                          // kernel stats
+    c.take<float>(static_cast<size_t>(egrad_floats(m, n_tokens, p)));
     size_t b = c.used();
     if (p->mode == 1) b += sync_extra_bytes(m->V, m->dim, std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len)));
     return b;
@@ -225,7 +239,7 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     if (p->cache_k > m->V - 1) return fail(W2V_E_ARG, "cache_k must be <= V-1");
     const size_t lds = train_lds_bytes(p->cache_k, m->dim);
     if (lds + 1024 > device_max_lds())
-        return fail(W2V_E_ARG, "cache does not fit LDS: 2*cache_k*dim*4 = " + std::to_string(lds) + " bytes");
+        return fail(W2V_E_ARG, "cache does not fit LDS: 2 * cache_k rows = " + std::to_string(lds) + " bytes");
     if (int rc = check_ws(workspace, workspace_bytes, train_bytes(m, n_tokens, p))) return rc;
     hipStream_t s = as_stream(hip_stream);
     Carve c(workspace);
@@ -234,6 +248,8 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     float *alpha_tab = c.take<float>(static_cast<size_t>(span / 10000 + 3));
     int32_t *queue = c.take<int32_t>(4);
     unsigned long long *tstats = c.take<unsigned long long>(4);
+    const int64_t n_egrad = egrad_floats(m, n_tokens, p);
+    float *egrad = c.take<float>(static_cast<size_t>(n_egrad));
 
     if (int rc = launch_sampling(tokens, n_tokens, m->V, m->vocab_counts, m->train_words, p, b, nullptr, s)) return rc;
     const int64_t eb = static_cast<int64_t>(p->epoch) * p->corpus_tokens;
@@ -273,12 +289,14 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     a.blk0 = blk0;
     a.cache_k = p->cache_k;
     a.cache_first = m->V - 1 - p->cache_k;
+    a.atomic_first = static_cast<int32_t>(std::max<int64_t>(0, static_cast<int64_t>(a.cache_first) - p->hot_k));
     a.flush_every = p->flush_every;
     a.workers = p->workers;
     a.write_policy = p->write_policy;
     a.flush_scale = p->flush_policy == 1 ? 0.0f : 1.0f;   // 0: set to 1 / workgroups at launch
     a.queue = queue;
     a.stats = tstats;
+    a.egrad = n_egrad > 0 ? egrad : nullptr;
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     if (int rc = timing_events(&ev0, &ev1)) return rc;
     return launch_train_async(a, p->arch, p->window, ev0, ev1, s, stats, b.totals);

@@ -110,11 +110,23 @@ __device__ __forceinline__ void load_row(float (&r)[NE], const float *__restrict
     }
 }
 
-// LDS row with zero padding up to NE*64 columns.
+// Cached rows in LDS. Up to 8 elements per lane they are padded with zeros to
+// NE*64 columns, so that whole rows are read and added without lane masks; the
+// widest variant keeps them dim floats apart to fit 2 cache_k rows in LDS.
 template <int NE>
-__device__ __forceinline__ void load_row_lds(float (&r)[NE], const float *p, int lane) {
+constexpr bool pad_lds() { return NE <= 8; }
+
+template <int NE>
+__host__ __device__ __forceinline__ int lds_stride(int dim) { return pad_lds<NE>() ? NE * kWave : dim; }
+
+template <int NE>
+__device__ __forceinline__ void load_row_lds(float (&r)[NE], const float *p, int lane, int dim) {
+    if constexpr (pad_lds<NE>()) {
 #pragma unroll
-    for (int i = 0; i < NE; ++i) r[i] = p[lane + i * kWave];
+        for (int i = 0; i < NE; ++i) r[i] = p[lane + i * kWave];
+    } else {
+        load_row<NE>(r, p, lane, dim);
+    }
 }
 
 // Row writes. With full rows (row_stride >= NE*64) all NE*64 columns are written
@@ -165,7 +177,8 @@ __device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainAr
     for (int j = 0; j < kChunk; ++j) {
         if (c0 + j < len) {
             const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-            if (n >= a.cache_first) load_row_lds<NE>(y[j], val + (n - a.cache_first) * (NE * kWave), lane);
+            if (n >= a.cache_first)
+                load_row_lds<NE>(y[j], val + (n - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
             else load_row<NE>(y[j], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
         } else {
             zero_row<NE>(y[j]);
@@ -173,81 +186,163 @@ __device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainAr
     }
 }
 
-// Walk the path of the centre with the inputs x[0..nx) (in order), accumulating
-// the hidden-layer gradients into e[0..nx). PG = compile-time bound of nx.
-template <int NE, int PG, bool PREFETCH>
-__device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const float (&x)[PG][NE],
-                                          float (&e)[PG][NE], int nx, int my_pt, int len, uint64_t code, float alpha,
-                                          int lane) {
-    float yc[kChunk][NE], yn[kChunk][NE], y0[kChunk][NE];
-    load_chunk<NE>(yc, a, val, my_pt, 0, len, lane);
-    const int row = lane >> 4;
-    for (int c0 = 0; c0 < len; c0 += kChunk) {
-        if (PREFETCH && c0 + kChunk < len) load_chunk<NE>(yn, a, val, my_pt, c0 + kChunk, len, lane);
+// Rows of nodes c0 .. c0+3 of the path, all outside the cache (zeros past its end).
+template <int NE>
+__device__ __forceinline__ void load_chunk_hbm(float (&y)[kChunk][NE], const TrainArgs &a, int my_pt, int c0, int len,
+                                               int lane) {
 #pragma unroll
-        for (int j = 0; j < kChunk; ++j)
+    for (int j = 0; j < kChunk; ++j) {
+        if (c0 + j < len) {
+            const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
+            load_row<NE>(y[j], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
+        } else {
+            zero_row<NE>(y[j]);
+        }
+    }
+}
+
+// Every input x[0..nx), in order, updates the nc live rows of the chunk held in
+// yc (dot, sigmoid, gradient, then e += g y and y += g x for each row).
+template <int NE, int PG>
+__device__ __forceinline__ void chunk_update(float (&yc)[kChunk][NE], const float (&x)[PG][NE], float (&e)[PG][NE],
+                                             int nx, int nc, int c0, uint64_t code, float alpha, int lane) {
+    const int bitpos = c0 + (lane >> 4);
+    const float t = (bitpos < 64) ? static_cast<float>((code >> bitpos) & 1ull) : 0.0f;
+    const float one_minus_t = 1.0f - t;
 #pragma unroll
-            for (int i = 0; i < NE; ++i) y0[j][i] = yc[j][i];
-        const int bitpos = c0 + row;
-        const float t = (bitpos < 64) ? static_cast<float>((code >> bitpos) & 1ull) : 0.0f;
-        const float one_minus_t = 1.0f - t;
-        const int nc = min(kChunk, len - c0);
+    for (int p = 0; p < PG; ++p) {
+        if (p < nx) {
+            const float z = reduce4(dot_partial<NE>(x[p], yc[0]), dot_partial<NE>(x[p], yc[1]),
+                                    dot_partial<NE>(x[p], yc[2]), dot_partial<NE>(x[p], yc[3]));
+            const float gr = (one_minus_t - sigmoid_fast(z)) * alpha;
 #pragma unroll
-        for (int p = 0; p < PG; ++p) {
-            if (p < nx) {
-                const float z = reduce4(dot_partial<NE>(x[p], yc[0]), dot_partial<NE>(x[p], yc[1]),
-                                        dot_partial<NE>(x[p], yc[2]), dot_partial<NE>(x[p], yc[3]));
-                const float gr = (one_minus_t - sigmoid_fast(z)) * alpha;
+            for (int j = 0; j < kChunk; ++j) {
+                if (j < nc) {
+                    const float gj =
+                        __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gr), 16 * j));
 #pragma unroll
-                for (int j = 0; j < kChunk; ++j) {
-                    if (j < nc) {
-                        const float gj = __builtin_bit_cast(
-                            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gr), 16 * j));
-#pragma unroll
-                        for (int i = 0; i < NE; ++i) {
-                            e[p][i] = fmaf(gj, yc[j][i], e[p][i]);
-                            yc[j][i] = fmaf(gj, x[p][i], yc[j][i]);
-                        }
+                    for (int i = 0; i < NE; ++i) {
+                        e[p][i] = fmaf(gj, yc[j][i], e[p][i]);
+                        yc[j][i] = fmaf(gj, x[p][i], yc[j][i]);
                     }
                 }
             }
         }
-        // write the change of each row back once
+    }
+}
+
+// Write-back of a chunk from its change yc - y0: LDS atomic add for cached rows,
+// HBM store of the new row (write_policy bit 0) or atomic add of the change.
+template <int NE>
+__device__ __forceinline__ void chunk_write_delta(const TrainArgs &a, float *val, const float (&yc)[kChunk][NE],
+                                                  const float (&y0)[kChunk][NE], int my_pt, int c0, int nc, int lane) {
 #pragma unroll
-        for (int j = 0; j < kChunk; ++j) {
-            if (j < nc) {
-                const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-                float d[NE];
+    for (int j = 0; j < kChunk; ++j) {
+        if (j < nc) {
+            const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
+            float d[NE];
 #pragma unroll
-                for (int i = 0; i < NE; ++i) d[i] = yc[j][i] - y0[j][i];
-                if (n >= a.cache_first) {
-                    float *lrow = val + (n - a.cache_first) * (NE * kWave);
+            for (int i = 0; i < NE; ++i) d[i] = yc[j][i] - y0[j][i];
+            if (n >= a.cache_first) {
+                float *lrow = val + (n - a.cache_first) * lds_stride<NE>(a.dim);
 #pragma unroll
-                    for (int i = 0; i < NE; ++i) lds_add(lrow + lane + i * kWave, d[i]);
-                } else {
-                    float *grow = a.syn1 + static_cast<int64_t>(n) * a.stride;
-                    if (a.write_policy & 1) store_row<NE>(grow, yc[j], lane, a.dim, a.full_rows);
-                    else atomic_add_row<NE>(grow, d, lane, a.dim, a.full_rows);
-                }
+                for (int i = 0; i < NE; ++i)
+                    if (pad_lds<NE>() || lane + i * kWave < a.dim) lds_add(lrow + lane + i * kWave, d[i]);
+            } else {
+                float *grow = a.syn1 + static_cast<int64_t>(n) * a.stride;
+                if ((a.write_policy & 1) && n < a.atomic_first) store_row<NE>(grow, yc[j], lane, a.dim, a.full_rows);
+                else atomic_add_row<NE>(grow, d, lane, a.dim, a.full_rows);
             }
         }
-        if (c0 + kChunk < len) {
-            if (PREFETCH) {
+    }
+}
+
+// Prefetch modes of the path walk.
+//   kPfNone   : each chunk is loaded after the previous one is written back.
+//   kPfAll    : the next chunk is loaded while the current one is updated.
+//   kPfSuffix : the path's cached and hot nodes form a prefix (an inner node is
+//               created after its children, so indices fall from the root down
+//               and the top indices sit at the top of every path). Chunks that
+//               hold such a row keep their loaded values (y0) to form the
+//               change; the chunks after them, when rows are written back by
+//               plain stores, need no copy, and those registers hold the
+//               prefetched next chunk instead.
+constexpr int kPfNone = 0, kPfAll = 1, kPfSuffix = 2;
+
+// Walk the path of the centre with the inputs x[0..nx) (in order), accumulating
+// the hidden-layer gradients into e[0..nx). PG = compile-time bound of nx.
+template <int NE, int PG, int PF>
+__device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const float (&x)[PG][NE],
+                                          float (&e)[PG][NE], int nx, int my_pt, int len, uint64_t code, float alpha,
+                                          int lane) {
+    float yc[kChunk][NE], y0[kChunk][NE];
+    if constexpr (PF == kPfAll) {
+        float yn[kChunk][NE];
+        load_chunk<NE>(yc, a, val, my_pt, 0, len, lane);
+        for (int c0 = 0; c0 < len; c0 += kChunk) {
+            if (c0 + kChunk < len) load_chunk<NE>(yn, a, val, my_pt, c0 + kChunk, len, lane);
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+                for (int i = 0; i < NE; ++i) y0[j][i] = yc[j][i];
+            const int nc = min(kChunk, len - c0);
+            chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+            chunk_write_delta<NE>(a, val, yc, y0, my_pt, c0, nc, lane);
+            if (c0 + kChunk < len) {
 #pragma unroll
                 for (int j = 0; j < kChunk; ++j)
 #pragma unroll
                     for (int i = 0; i < NE; ++i) yc[j][i] = yn[j][i];
-            } else {
-                load_chunk<NE>(yc, a, val, my_pt, c0 + kChunk, len, lane);
+            }
+        }
+        return;
+    }
+    int end_delta = len;   // chunks starting below this keep y0
+    if constexpr (PF == kPfSuffix) {
+        if (a.write_policy & 1) {
+            const uint64_t kept = __ballot(lane < len && my_pt >= a.atomic_first);
+            end_delta = __popcll(kept);
+        }
+    }
+    int c0 = 0;
+    for (; c0 < end_delta; c0 += kChunk) {
+        load_chunk<NE>(yc, a, val, my_pt, c0, len, lane);
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+            for (int i = 0; i < NE; ++i) y0[j][i] = yc[j][i];
+        const int nc = min(kChunk, len - c0);
+        chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+        chunk_write_delta<NE>(a, val, yc, y0, my_pt, c0, nc, lane);
+    }
+    if constexpr (PF == kPfSuffix) {
+        // uncached rows only, written back by stores; y0's registers carry the next chunk
+        if (c0 < len) load_chunk_hbm<NE>(yc, a, my_pt, c0, len, lane);
+        for (; c0 < len; c0 += kChunk) {
+            if (c0 + kChunk < len) load_chunk_hbm<NE>(y0, a, my_pt, c0 + kChunk, len, lane);
+            const int nc = min(kChunk, len - c0);
+            chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j) {
+                if (j < nc) {
+                    const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
+                    store_row<NE>(a.syn1 + static_cast<int64_t>(n) * a.stride, yc[j], lane, a.dim, a.full_rows);
+                }
+            }
+            if (c0 + kChunk < len) {
+#pragma unroll
+                for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) yc[j][i] = y0[j][i];
             }
         }
     }
 }
 
 // ARCH 0: skip-gram, window words in groups of PG; ARCH 1: CBOW (one input, the mean).
-template <int NE, int PG, int ARCH, int WPB, bool PREFETCH>
+template <int NE, int PG, int ARCH, int WPB, int PF>
 __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
-    constexpr int LS = NE * kWave;   // LDS row stride (zero padding past dim)
+    const int LS = lds_stride<NE>(a.dim);
     extern __shared__ float lds[];
     float *val = lds;
     float *orig = lds + a.cache_k * LS;
@@ -300,7 +395,12 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
 
                     if constexpr (ARCH == 0) {
-                        // groups of PG window words walk the path in turn (one group when P <= PG)
+                        // groups of PG window words walk the path in turn (one group when P <= PG). With
+                        // several groups the hidden-layer gradients are parked in the wavefront's egrad
+                        // rows and added to syn0 after the last group, so that every group reads the
+                        // window vectors as they were before this centre (as a single walk does).
+                        const bool defer = P > PG;
+                        float *eg = a.egrad + static_cast<int64_t>(gw) * a.egrad_slots * a.stride;
                         for (int g0 = 0; g0 < P; g0 += PG) {
                             const int nx = min(PG, P - g0);
                             float x[PG][NE], e[PG][NE];
@@ -314,7 +414,14 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                                 }
                                 zero_row<NE>(e[p]);
                             }
-                            walk_path<NE, PG, PREFETCH>(a, val, x, e, nx, my_pt, len, code, alpha, lane);
+                            walk_path<NE, PG, PF>(a, val, x, e, nx, my_pt, len, code, alpha, lane);
+                            if (defer) {
+#pragma unroll
+                                for (int p = 0; p < PG; ++p)
+                                    if (p < nx) store_row<NE>(eg + static_cast<int64_t>(g0 + p) * a.stride, e[p],
+                                                              lane, a.dim, a.full_rows);
+                                continue;
+                            }
 #pragma unroll
                             for (int p = 0; p < PG; ++p) {
                                 if (p < nx) {
@@ -328,6 +435,23 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                                     } else {
                                         atomic_add_row<NE>(xr, e[p], lane, a.dim, a.full_rows);
                                     }
+                                }
+                            }
+                        }
+                        if (defer) {
+                            for (int q = 0; q < P; ++q) {
+                                const int w = __builtin_amdgcn_readlane(wv, q);
+                                float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
+                                float eq[NE];
+                                load_row<NE>(eq, eg + static_cast<int64_t>(q) * a.stride, lane, a.dim);
+                                if (a.write_policy & 2) {
+                                    float cur[NE];
+                                    load_row<NE>(cur, xr, lane, a.dim);
+#pragma unroll
+                                    for (int i = 0; i < NE; ++i) cur[i] += eq[i];
+                                    store_row<NE>(xr, cur, lane, a.dim, a.full_rows);
+                                } else {
+                                    atomic_add_row<NE>(xr, eq, lane, a.dim, a.full_rows);
                                 }
                             }
                         }
@@ -347,7 +471,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                         const float fP = static_cast<float>(P);
 #pragma unroll
                         for (int i = 0; i < NE; ++i) h[0][i] = h[0][i] / fP;
-                        walk_path<NE, 1, PREFETCH>(a, val, h, e, 1, my_pt, len, code, alpha, lane);
+                        walk_path<NE, 1, PF>(a, val, h, e, 1, my_pt, len, code, alpha, lane);
                         for (int p = 0; p < P; ++p) {
                             const int w = __builtin_amdgcn_readlane(wv, p);
                             float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
@@ -398,13 +522,15 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
 struct Variant {
     void (*fn)(TrainArgs);
     int waves_per_block;
-    int ne;
+    int ne;   // elements per lane
+    int pg;   // window words per path walk (skip-gram)
+    int (*ls)(int);
 };
 
-template <int NE, int PG, int WPB, bool PF>
+template <int NE, int PG, int WPB, int PF>
 Variant variant(int arch) {
-    if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE};
-    return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE};
+    if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE, PG, lds_stride<NE>};
+    return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE, 1, lds_stride<NE>};
 }
 
 // Register budget per lane: x and e take 2*PG*NE, the chunk rows 2 (3 with the
@@ -412,12 +538,12 @@ Variant variant(int arch) {
 // without the prefetch ran 21 % faster than 2 with it.
 Variant pick_variant(int arch, int dim) {
     const int ne = (dim + kWave - 1) / kWave;
-    if (ne <= 1) return variant<1, 20, 16, true>(arch);
-    if (ne <= 2) return variant<2, 20, 12, true>(arch);
-    if (ne <= 4) return variant<4, 10, 12, true>(arch);
-    if (ne <= 5) return variant<5, 10, 12, false>(arch);
-    if (ne <= 8) return variant<8, 4, 8, false>(arch);
-    return variant<16, 2, 8, false>(arch);
+    if (ne <= 1) return variant<1, 20, 16, kPfAll>(arch);
+    if (ne <= 2) return variant<2, 20, 12, kPfAll>(arch);
+    if (ne <= 4) return variant<4, 10, 12, kPfAll>(arch);
+    if (ne <= 5) return variant<5, 10, 12, kPfSuffix>(arch);
+    if (ne <= 8) return variant<8, 4, 8, kPfSuffix>(arch);
+    return variant<16, 2, 8, kPfSuffix>(arch);
 }
 
 __global__ void k_zero_train(int32_t *queue, unsigned long long *stats) {
@@ -438,34 +564,52 @@ __global__ void k_write_stats(const int64_t *totals, const unsigned long long *t
 }  // namespace
 
 size_t train_lds_bytes(int32_t cache_k, int32_t dim) {
-    const int ne = (dim + kWave - 1) / kWave;
-    const int ne_v = ne <= 2 ? ne : (ne <= 4 ? 4 : (ne <= 5 ? 5 : (ne <= 8 ? 8 : 16)));
-    return 2ull * cache_k * ne_v * kWave * sizeof(float);
+    const Variant v = pick_variant(0, dim);
+    return 2ull * cache_k * v.ls(dim) * sizeof(float);
+}
+
+int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_docs, int *grid, int *waves) {
+    const Variant v = pick_variant(arch, dim);
+    if (workers > 0) {
+        *grid = static_cast<int>(ceil_div(workers, v.waves_per_block));
+        *waves = workers;
+        return W2V_OK;
+    }
+    const size_t lds = 2ull * cache_k * v.ls(dim) * sizeof(float);
+    int per_cu = 0;
+    W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(v.fn),
+                                                         v.waves_per_block * kWave, lds));
+    int64_t g = static_cast<int64_t>(device_cu_count()) * std::max(1, per_cu);
+    // every wavefront gets at least kMinDocsPerWave documents, so that every workgroup
+    // (cache owner) contributes to the averaged write-back of the cached rows
+    const int64_t by_docs = ceil_div(n_docs, static_cast<int64_t>(v.waves_per_block) * kMinDocsPerWave);
+    g = std::max<int64_t>(1, std::min<int64_t>(g, by_docs));
+    *grid = static_cast<int>(g);
+    *waves = *grid * v.waves_per_block;
+    return W2V_OK;
+}
+
+int64_t train_egrad_floats(int arch, int dim, int stride, int window, int waves) {
+    const Variant v = pick_variant(arch, dim);
+    if (arch != 0 || 2 * window <= v.pg) return 0;
+    return static_cast<int64_t>(waves) * 2 * window * stride;
 }
 
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals) {
-    (void)window;
     const Variant v = pick_variant(arch, a.dim);
-    const size_t lds = 2ull * a.cache_k * v.ne * kWave * sizeof(float);
+    const size_t lds = 2ull * a.cache_k * v.ls(a.dim) * sizeof(float);
     const int block = v.waves_per_block * kWave;
     a.full_rows = a.stride >= v.ne * kWave ? 1 : 0;
     if (lds > 64 * 1024)
         W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(v.fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(lds)));
-    int grid;
-    if (a.workers > 0) {
-        grid = static_cast<int>(ceil_div(a.workers, v.waves_per_block));
-    } else {
-        int per_cu = 0;
-        W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(v.fn), block,
-                                                             lds));
-        grid = device_cu_count() * std::max(1, per_cu);
-        // every wavefront gets at least kMinDocsPerWave documents, so that every workgroup
-        // (cache owner) contributes to the averaged write-back of the cached rows
-        const int64_t by_docs = ceil_div(a.n_docs, static_cast<int64_t>(v.waves_per_block) * kMinDocsPerWave);
-        grid = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(grid, by_docs)));
-        a.workers = grid * v.waves_per_block;
+    int grid = 0, waves = 0;
+    if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.workers, a.n_docs, &grid, &waves)) return rc;
+    a.workers = waves;
+    if (train_egrad_floats(arch, a.dim, a.stride, window, waves) > 0) {
+        if (!a.egrad) return fail(W2V_E_ARG, "internal: egrad rows missing");
+        a.egrad_slots = 2 * window;
     }
     if (a.flush_scale <= 0.0f) a.flush_scale = 1.0f / static_cast<float>(grid);
     record_train_launch(grid, a.workers);

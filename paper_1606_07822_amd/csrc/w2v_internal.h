@@ -153,12 +153,15 @@ struct TrainArgs {
     const float *alpha_tab;
     int64_t blk0;
     int32_t cache_k, cache_first, flush_every;
+    int32_t atomic_first;    // uncached rows from here up take atomic adds even under the store policy
     int32_t workers;
     int32_t write_policy;
     int32_t full_rows;       // row_stride covers the variant's NE*64 columns: whole-row writes
     float flush_scale;       // fraction of the cached rows' change written back (1 = all of it)
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, node updates
+    float *egrad;            // per wavefront egrad_slots rows of row_stride floats (parked gradients), or null
+    int32_t egrad_slots;
 };
 
 }  // namespace w2v

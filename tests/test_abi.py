@@ -43,6 +43,7 @@ def test_struct_layouts_match_header(w2v):
     assert w2v.CModel.points.offset == 72 and ctypes.sizeof(w2v.CModel) == 80
     assert w2v.CParams.sample.offset == 16 and w2v.CParams.corpus_tokens.offset == 40
     assert w2v.CParams.seed.offset == 56 and w2v.CParams.write_policy.offset == 80
+    assert w2v.CParams.hot_k.offset == 88
     assert ctypes.sizeof(w2v.CParams) == 112
 
 
@@ -112,6 +113,9 @@ def _params(w2v, **kw):
     ({}, dict(cache_k=-1), "cache_k"),
     ({}, dict(cache_k=100), "cache_k"),
     ({}, dict(alpha0=0.0), "alpha0"),
+    ({}, dict(hot_k=-1), "hot_k"),
+    ({}, dict(write_policy=4), "write_policy"),
+    ({}, dict(flush_policy=2), "flush_policy"),
 ])
 def test_train_argument_errors(w2v, mk, pk, msg):
     L = w2v.lib()

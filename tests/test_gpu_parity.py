@@ -258,21 +258,33 @@ def test_sync_mode_is_deterministic(w2v):
 
 
 # ------------------------------------------------------------- asynchronous mode
-@pytest.mark.parametrize("arch,k,F,ndocs", [(0, 0, 10, 5), (0, 31, 10, 5), (0, 7, 1, 5), (1, 0, 10, 5),
-                                             (1, 31, 10, 5)])
-def test_single_worker_matches_oracle_centre_major(w2v, arch, k, F, ndocs):
+# One wavefront reproduces the oracle's centre-major order up to rounding. dim picks the kernel variant
+# (elements per lane 2, 4, 5, 8, 16; up to 256 columns every chunk is prefetched, above only past the
+# cached prefix); write_policy 0 (atomic adds of the change) and 1 (row stores) take different write-back
+# paths; window 10 gives skip-gram windows wider than one register group at dim >= 200 (parked gradients).
+@pytest.mark.parametrize("arch,k,F,ndocs,dim,wp,win", [
+    (0, 0, 10, 5, 100, 1, 5), (0, 31, 10, 5, 100, 1, 5), (0, 7, 1, 5, 100, 1, 5), (1, 0, 10, 5, 100, 1, 5),
+    (1, 31, 10, 5, 100, 1, 5),
+    (0, 0, 10, 3, 300, 1, 5), (0, 31, 10, 3, 300, 1, 5), (0, 31, 10, 3, 300, 0, 5), (1, 0, 10, 3, 300, 1, 5),
+    (1, 31, 10, 3, 300, 1, 5), (1, 31, 10, 3, 300, 0, 5),
+    (0, 31, 10, 2, 300, 1, 10), (0, 31, 10, 2, 300, 0, 10), (1, 31, 10, 2, 300, 1, 10),
+    (0, 31, 10, 2, 200, 1, 10), (0, 31, 10, 2, 450, 1, 5), (1, 31, 10, 2, 450, 1, 5), (0, 31, 10, 2, 600, 1, 5),
+    (1, 31, 10, 2, 600, 1, 5), (0, 15, 10, 2, 1024, 0, 3),
+])
+def test_single_worker_matches_oracle_centre_major(w2v, arch, k, F, ndocs, dim, wp, win):
+    log(f"single worker arch={arch} k={k} F={F} docs={ndocs} dim={dim} write_policy={wp} window={win}")
     s = oracle_side("sg_v30k_d100")
     voc, tree = gpu_side(w2v, s)
     tv = s.tv[:ndocs * 1000]
-    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim, syn1_scale=0.5 / s.w.dim)
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
     a0, a1 = syn0.copy(), syn1.copy()
     alpha0 = 0.05 if arch else 0.025
-    op = oracle.params(s.voc.V, s.w.dim, window=5, sample=1e-3, train_words=s.voc.train_words,
+    op = oracle.params(s.voc.V, dim, window=win, sample=1e-3, train_words=s.voc.train_words,
                        corpus_tokens=s.tv.size, cache_k=k, flush_every=F, order=1, arch=arch, alpha0=alpha0)
     ost = oracle.train(a0, a1, s.tree, tv, op)
     model = w2v.make_model(syn0, syn1, voc, tree)
-    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, cache_k=k, flush_every=F, workers=1, arch=arch,
-                   alpha0=alpha0)
+    p = w2v.Params(window=win, sample=1e-3, corpus_tokens=s.tv.size, cache_k=k, flush_every=F, workers=1, arch=arch,
+                   alpha0=alpha0, write_policy=wp)
     st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
     assert list(st) == list(ost)
     g0, g1 = (t.cpu().numpy() for t in model.vectors())
