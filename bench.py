@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--cache-k", type=int, default=31)
     ap.add_argument("--flush-every", type=int, default=1000)
     ap.add_argument("--flush-policy", type=int, default=1)
-    ap.add_argument("--write-policy", type=int, default=1)
+    ap.add_argument("--write-policy", type=int, default=5)
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
     ap.add_argument("--copy-calibration", action="store_true",

@@ -258,7 +258,7 @@ class Params:
     flush_every: int = 1000
     sync_batch: int = 4096
     workers: int = 0
-    write_policy: int = 1
+    write_policy: int = 5
     flush_policy: int = 1
     hot_k: int | None = None
     extra: dict = field(default_factory=dict)

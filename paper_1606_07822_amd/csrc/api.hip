@@ -117,7 +117,7 @@ int check_params(const w2v_params *p, bool training) {
         if (p->flush_every < 1) return fail(W2V_E_ARG, "flush_every must be >= 1");
         if (p->mode == 1 && p->sync_batch < 1) return fail(W2V_E_ARG, "sync_batch must be >= 1");
         if (p->workers < 0) return fail(W2V_E_ARG, "workers must be >= 0");
-        if (p->write_policy < 0 || p->write_policy > 3) return fail(W2V_E_ARG, "write_policy must be in 0..3");
+        if (p->write_policy < 0 || p->write_policy > 7) return fail(W2V_E_ARG, "write_policy must be in 0..7");
         if (p->flush_policy != 0 && p->flush_policy != 1) return fail(W2V_E_ARG, "flush_policy must be 0 or 1");
         if (p->hot_k < 0) return fail(W2V_E_ARG, "hot_k must be >= 0");
     }

@@ -19,7 +19,8 @@
 // Cache (§3.2): the cache owner is the workgroup. The rows of the top
 // cache_k inner nodes (the k created last by the Huffman merge) sit in LDS as
 // `val` (current) and `orig` (value at the last write-back); waves update
-// `val` with LDS atomic adds of their change. Every flush_every centres of the
+// `val` with LDS atomic adds of their change, or (write_policy bit 2) store
+// their new row into it, lock-free like the HBM rows. Every flush_every centres of the
 // workgroup, one wave writes flush_scale * (val - orig) back to HBM with an
 // atomic add and re-bases both copies on the returned HBM value (write-back
 // plus refill, without stopping the other waves).
@@ -129,6 +130,13 @@ __device__ __forceinline__ void load_row_lds(float (&r)[NE], const float *p, int
     }
 }
 
+template <int NE>
+__device__ __forceinline__ void store_row_lds(float *p, const float (&r)[NE], int lane, int dim) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i)
+        if (pad_lds<NE>() || lane + i * kWave < dim) p[lane + i * kWave] = r[i];
+}
+
 // Row writes. With full rows (row_stride >= NE*64) all NE*64 columns are written
 // (the padding columns receive zeros / zero changes) and no lane is masked.
 template <int NE>
@@ -186,21 +194,6 @@ __device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainAr
     }
 }
 
-// Rows of nodes c0 .. c0+3 of the path, all outside the cache (zeros past its end).
-template <int NE>
-__device__ __forceinline__ void load_chunk_hbm(float (&y)[kChunk][NE], const TrainArgs &a, int my_pt, int c0, int len,
-                                               int lane) {
-#pragma unroll
-    for (int j = 0; j < kChunk; ++j) {
-        if (c0 + j < len) {
-            const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-            load_row<NE>(y[j], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
-        } else {
-            zero_row<NE>(y[j]);
-        }
-    }
-}
-
 // Every input x[0..nx), in order, updates the nc live rows of the chunk held in
 // yc (dot, sigmoid, gradient, then e += g y and y += g x for each row).
 template <int NE, int PG>
@@ -245,9 +238,13 @@ __device__ __forceinline__ void chunk_write_delta(const TrainArgs &a, float *val
             for (int i = 0; i < NE; ++i) d[i] = yc[j][i] - y0[j][i];
             if (n >= a.cache_first) {
                 float *lrow = val + (n - a.cache_first) * lds_stride<NE>(a.dim);
+                if (a.write_policy & 4) {
+                    store_row_lds<NE>(lrow, yc[j], lane, a.dim);
+                } else {
 #pragma unroll
-                for (int i = 0; i < NE; ++i)
-                    if (pad_lds<NE>() || lane + i * kWave < a.dim) lds_add(lrow + lane + i * kWave, d[i]);
+                    for (int i = 0; i < NE; ++i)
+                        if (pad_lds<NE>() || lane + i * kWave < a.dim) lds_add(lrow + lane + i * kWave, d[i]);
+                }
             } else {
                 float *grow = a.syn1 + static_cast<int64_t>(n) * a.stride;
                 if ((a.write_policy & 1) && n < a.atomic_first) store_row<NE>(grow, yc[j], lane, a.dim, a.full_rows);
@@ -263,10 +260,11 @@ __device__ __forceinline__ void chunk_write_delta(const TrainArgs &a, float *val
 //   kPfSuffix : the path's cached and hot nodes form a prefix (an inner node is
 //               created after its children, so indices fall from the root down
 //               and the top indices sit at the top of every path). Chunks that
-//               hold such a row keep their loaded values (y0) to form the
-//               change; the chunks after them, when rows are written back by
-//               plain stores, need no copy, and those registers hold the
-//               prefetched next chunk instead.
+//               hold a row written back as a change (atomic add) keep their
+//               loaded values (y0); the chunks after them, whose rows are
+//               stored, need no copy, and those registers hold the prefetched
+//               next chunk instead. With every row stored the whole path is
+//               prefetched.
 constexpr int kPfNone = 0, kPfAll = 1, kPfSuffix = 2;
 
 // Walk the path of the centre with the inputs x[0..nx) (in order), accumulating
@@ -300,7 +298,9 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
     int end_delta = len;   // chunks starting below this keep y0
     if constexpr (PF == kPfSuffix) {
         if (a.write_policy & 1) {
-            const uint64_t kept = __ballot(lane < len && my_pt >= a.atomic_first);
+            // changes are needed for hot rows (atomic adds) and for cached rows unless those are stored
+            const bool adds = !(a.write_policy & 4) || a.atomic_first < a.cache_first;
+            const uint64_t kept = __ballot(adds && lane < len && my_pt >= a.atomic_first);
             end_delta = __popcll(kept);
         }
     }
@@ -316,17 +316,20 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
         chunk_write_delta<NE>(a, val, yc, y0, my_pt, c0, nc, lane);
     }
     if constexpr (PF == kPfSuffix) {
-        // uncached rows only, written back by stores; y0's registers carry the next chunk
-        if (c0 < len) load_chunk_hbm<NE>(yc, a, my_pt, c0, len, lane);
+        // rows written back by stores (LDS for cached rows); y0's registers carry the next chunk
+        if (c0 < len) load_chunk<NE>(yc, a, val, my_pt, c0, len, lane);
         for (; c0 < len; c0 += kChunk) {
-            if (c0 + kChunk < len) load_chunk_hbm<NE>(y0, a, my_pt, c0 + kChunk, len, lane);
+            if (c0 + kChunk < len) load_chunk<NE>(y0, a, val, my_pt, c0 + kChunk, len, lane);
             const int nc = min(kChunk, len - c0);
             chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
 #pragma unroll
             for (int j = 0; j < kChunk; ++j) {
                 if (j < nc) {
                     const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-                    store_row<NE>(a.syn1 + static_cast<int64_t>(n) * a.stride, yc[j], lane, a.dim, a.full_rows);
+                    if (n >= a.cache_first)
+                        store_row_lds<NE>(val + (n - a.cache_first) * lds_stride<NE>(a.dim), yc[j], lane, a.dim);
+                    else
+                        store_row<NE>(a.syn1 + static_cast<int64_t>(n) * a.stride, yc[j], lane, a.dim, a.full_rows);
                 }
             }
             if (c0 + kChunk < len) {

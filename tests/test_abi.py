@@ -114,7 +114,7 @@ def _params(w2v, **kw):
     ({}, dict(cache_k=100), "cache_k"),
     ({}, dict(alpha0=0.0), "alpha0"),
     ({}, dict(hot_k=-1), "hot_k"),
-    ({}, dict(write_policy=4), "write_policy"),
+    ({}, dict(write_policy=8), "write_policy"),
     ({}, dict(flush_policy=2), "flush_policy"),
 ])
 def test_train_argument_errors(w2v, mk, pk, msg):

@@ -260,8 +260,8 @@ def test_sync_mode_is_deterministic(w2v):
 # ------------------------------------------------------------- asynchronous mode
 # One wavefront reproduces the oracle's centre-major order up to rounding. dim picks the kernel variant
 # (elements per lane 2, 4, 5, 8, 16; up to 256 columns every chunk is prefetched, above only past the
-# cached prefix); write_policy 0 (atomic adds of the change) and 1 (row stores) take different write-back
-# paths; window 10 gives skip-gram windows wider than one register group at dim >= 200 (parked gradients).
+# cached prefix); write_policy 0 (atomic adds of the change), 1 (row stores) and 5 (row stores, cached rows
+# included) take different write-back paths; window 10 gives skip-gram windows wider than one register group at dim >= 200 (parked gradients).
 @pytest.mark.parametrize("arch,k,F,ndocs,dim,wp,win", [
     (0, 0, 10, 5, 100, 1, 5), (0, 31, 10, 5, 100, 1, 5), (0, 7, 1, 5, 100, 1, 5), (1, 0, 10, 5, 100, 1, 5),
     (1, 31, 10, 5, 100, 1, 5),
@@ -270,6 +270,8 @@ def test_sync_mode_is_deterministic(w2v):
     (0, 31, 10, 2, 300, 1, 10), (0, 31, 10, 2, 300, 0, 10), (1, 31, 10, 2, 300, 1, 10),
     (0, 31, 10, 2, 200, 1, 10), (0, 31, 10, 2, 450, 1, 5), (1, 31, 10, 2, 450, 1, 5), (0, 31, 10, 2, 600, 1, 5),
     (1, 31, 10, 2, 600, 1, 5), (0, 15, 10, 2, 1024, 0, 3),
+    (0, 31, 10, 5, 100, 5, 5), (0, 31, 10, 3, 300, 5, 5), (0, 31, 10, 2, 300, 5, 10), (1, 31, 10, 3, 300, 5, 5),
+    (0, 31, 10, 2, 450, 5, 5),
 ])
 def test_single_worker_matches_oracle_centre_major(w2v, arch, k, F, ndocs, dim, wp, win):
     log(f"single worker arch={arch} k={k} F={F} docs={ndocs} dim={dim} write_policy={wp} window={win}")
@@ -329,16 +331,19 @@ def golden(name):
 
 
 # Default asynchronous mode (top-31 cache in LDS, write-back of the workgroups' averaged change every
-# 1000 centres, Hogwild row stores elsewhere) at full occupancy; the same with atomic adds of the change
-# for uncached rows; no cache; and the cache with the paper's summed write-back, which is stable only
-# at low concurrency (256 wavefronts).
+# 1000 centres, Hogwild row stores in HBM and in the LDS copy) at full occupancy; the same with atomic adds
+# of the change everywhere (write_policy 0) or in LDS only (1); no cache; and the cache with the paper's
+# summed write-back, which is stable only at low concurrency (256 wavefronts). CBOW's default also adds
+# the change atomically on the 1024 hot rows below the cache.
 @pytest.mark.parametrize("name,kw", [
     ("sg_v30k_d100", {}),
     ("sg_v30k_d100", dict(write_policy=0)),
+    ("sg_v30k_d100", dict(write_policy=1)),
     ("sg_v30k_d100", dict(cache_k=0)),
     ("sg_v30k_d100", dict(workers=256, cache_k=31, flush_every=10, flush_policy=0, write_policy=0)),
     ("sg_v100k_d200", {}),
     ("sg_v100k_d200", dict(write_policy=0)),
+    ("sg_v100k_d200", dict(write_policy=1)),
     ("cbow_v100k_d300", {}),
 ])
 def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw):
