@@ -20,7 +20,6 @@ flush and at the end.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -46,20 +45,14 @@ def parse():
     ap.add_argument("--write-policy", type=int, default=5)
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
+    ap.add_argument("--no-probe", action="store_true", help="skip the random-row memory probe")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="run one 1 GiB device-to-device copy first (reference dispatch for HBM byte counters)")
+                    help="first write, then read, 1.28 GB of rows once each (reference dispatches for HBM byte counters)")
     return ap.parse_args()
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
-
-
-def kernel_source_hash() -> str:
-    h = hashlib.sha256()
-    for f in ("train.hip", "w2v_internal.h"):
-        h.update(open(os.path.join(ROOT, "paper_1606_07822_amd", "csrc", f), "rb").read())
-    return h.hexdigest()[:16]
 
 
 def algorithmic_bytes(torch, voc, tree, mask, doc_len, dim, k, flush_every, n_groups):
@@ -118,12 +111,18 @@ def main():
     ws = torch.empty(w2v.train_workspace_bytes(model, w.n_tokens, p), dtype=torch.uint8, device=dev)
     stats = torch.zeros(w2v.N_STATS, dtype=torch.int64, device=dev)
 
+    calib = None
     if args.copy_calibration:
-        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
+        # dispatches of known size for scaling the HBM byte counters: every row of a
+        # 1e6 x 320 float matrix written once, then read once (the training kernel's accesses)
+        rows, cols = 1_000_000, 320
+        m = torch.empty(rows, cols, dtype=torch.float32, device=dev)
+        iters = -(-rows // (256 * 12 * 4))
+        w2v.probe_rows(m, cols, 3, 256, iters)
+        w2v.probe_rows(m, cols, 2, 256, iters)
         torch.cuda.synchronize()
-        del src, dst
+        del m
+        calib = {"rows": rows, "row_bytes": 4 * cols, "write_dispatch": "k_probe<3, 5>", "read_dispatch": "k_probe<2, 5>"}
 
     # byte model of one launch (the sampler's keep mask with the training seed)
     pr = w2v.sample_pairs(voc.tokens, voc.V, voc.vocab_counts, voc.train_words, p, cap=0, want_mask=True)
@@ -175,8 +174,12 @@ def main():
     tfile = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
     if os.path.exists(tfile):
         t = json.load(open(tfile))
-        if t.get("kernel_source") == kernel_source_hash():
+        if t.get("kernel_source") == w2v.kernel_source_hash():
             traffic = t.get("hbm_bytes_per_launch")
+
+    # the training kernel moves whole padded rows (row_stride >= 64 * ceil(d / 64) floats) when it can
+    share = 64 * (-(-d // 64))
+    probe = None if args.no_probe else memory_probe(torch, w2v, voc.V, min(share, model.stride), model.stride, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -209,10 +212,32 @@ def main():
         "algorithmic_bytes_per_launch": byte_total,
         "heldout_mean_ll": (lls[-1][0] / lls[-1][1]) if lls and lls[-1] else None,
         "cpu_baseline": cpu,
-        "kernel_source": kernel_source_hash(),
+        "memory_probe": probe,
+        "counter_calibration": calib,
+        "kernel_source": w2v.kernel_source_hash(),
         "launch": {"workgroups": n_groups, "wavefronts": n_waves},
     }
     print(json.dumps(line), flush=True)
+
+
+def memory_probe(torch, w2v, rows, cols, stride, dev):
+    """Practical memory ceiling of the training kernel's access pattern: rows of
+    cols floats (the padded row the kernel moves; rows = V) at hashed positions,
+    four in flight per wavefront on the same launch shape, read and
+    read-modify-written."""
+    m = torch.zeros(rows, stride, dtype=torch.float32, device=dev)
+    wg, iters = 256, 1000
+    visits = wg * 12 * 4 * iters
+    out = {"rows": rows, "row_bytes": 4 * cols, "row_visits": visits}
+    for mode, name in ((0, "read"), (1, "rmw")):
+        w2v.probe_rows(m, cols, mode, wg, iters)                 # warm-up
+        ms = w2v.probe_rows(m, cols, mode, wg, iters)
+        moved = visits * 4 * cols * (2 if mode else 1)
+        out[f"{name}_GBps"] = moved / (ms / 1e3) / 1e9
+        out[f"{name}_rows_per_s"] = visits / (ms / 1e3)
+    del m
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(w, tok_np, args):
@@ -227,11 +252,12 @@ def cpu_baseline(w, tok_np, args):
     tree = oracle.build_huffman(voc.vocab_counts)
     log(f"oracle vocabulary + tree in {time.time() - t0:.1f}s")
     syn0, syn1 = synth.init_weights(voc.V, w.dim)
-    # calibrate on 2 documents, then size the sample to about cpu_seconds
-    n_cal = 2 * w.doc_len
-    tv = oracle.remap(tok_np[:n_cal], voc.id_to_vocab)
+    # calibrate on 20 documents (after 2 that warm the pages up), then size the sample to about cpu_seconds
     p = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, alpha0=w.alpha0, train_words=voc.train_words,
                       corpus_tokens=w.n_tokens, seed=synth.SEED_TRAIN, cache_k=31, flush_every=10, arch=w.arch)
+    oracle.train(syn0, syn1, tree, oracle.remap(tok_np[:2 * w.doc_len], voc.id_to_vocab), p)
+    n_cal = 20 * w.doc_len
+    tv = oracle.remap(tok_np[:n_cal], voc.id_to_vocab)
     t0 = time.perf_counter()
     oracle.train(syn0, syn1, tree, tv, p)
     per_tok = (time.perf_counter() - t0) / n_cal

@@ -227,6 +227,23 @@ int w2v_sample_pairs(const int32_t *tokens, int64_t n_tokens, int32_t V, const i
 int w2v_keep_thresholds(const int64_t *vocab_counts, int32_t V, double sample, int64_t train_words, uint64_t *thr,
                         void *hip_stream);
 
+/* ------------------------------------------------------------------------
+ * Measurement utility (not part of the method): the practical memory ceiling
+ * of the training kernel's access pattern. Wavefronts (12 per workgroup, four
+ * rows in flight each) visit rows of matrix (float[rows][row_stride], device
+ * memory, 16-byte aligned) picked by a 32-bit hash, iters times four rows
+ * each, and read the first cols floats (mode 0) or read them, add 1 and write
+ * them back (mode 1, the matrix is modified). Modes 2 and 3 visit rows
+ * 0, 1, 2, ... instead, each at most once (wavefront w, round i: rows
+ * 4 (w iters + i) .. +3), reading (2) or writing (3, the matrix is modified)
+ * the first cols floats: dispatches of known byte counts. ms_host: kernel time
+ * from HIP events on the stream. Synchronises the stream. Errors: W2V_E_ARG
+ * for NULL pointers, rows < 1, cols < 1 or > min(row_stride, 1024), mode
+ * not in 0..3, workgroups or iters < 1.
+ * ---------------------------------------------------------------------- */
+int w2v_probe_rows(float *matrix, int64_t rows, int32_t cols, int32_t row_stride, int32_t mode, int32_t workgroups,
+                   int32_t iters, float *ms_host, void *hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

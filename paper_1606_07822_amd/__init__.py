@@ -91,6 +91,8 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_size_t, P]
         L.w2v_keep_thresholds.restype = ctypes.c_int
         L.w2v_keep_thresholds.argtypes = [P, I32, ctypes.c_double, I64, P, P]
+        L.w2v_probe_rows.restype = ctypes.c_int
+        L.w2v_probe_rows.argtypes = [P, I64, I32, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_float), P]
         _LIB = L
     return _LIB
 
@@ -368,3 +370,23 @@ def keep_thresholds(vocab_counts: torch.Tensor, sample: float, train_words: int)
     _check(lib().w2v_keep_thresholds(_dev_ptr(vocab_counts, torch.int64, "vocab_counts"), V, float(sample),
                                      train_words, thr.data_ptr(), _stream(vocab_counts.device)))
     return thr
+
+
+def kernel_source_hash() -> str:
+    """First 16 hex digits of sha256 over the training kernel's sources (ties stored counter data to a build)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("train.hip", "w2v_internal.h"):
+        with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def probe_rows(matrix: torch.Tensor, cols: int, mode: int, workgroups: int = 256, iters: int = 1000) -> float:
+    """Kernel milliseconds of w2v_probe_rows over a float32 [rows, row_stride] GPU matrix."""
+    if matrix.dim() != 2:
+        raise ValueError("matrix must be 2-D")
+    ms = ctypes.c_float(0.0)
+    _check(lib().w2v_probe_rows(_dev_ptr(matrix, torch.float32, "matrix"), matrix.shape[0], cols, matrix.shape[1],
+                                mode, workgroups, iters, ctypes.byref(ms), _stream(matrix.device)))
+    return ms.value

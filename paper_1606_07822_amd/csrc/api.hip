@@ -27,6 +27,8 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
 size_t sync_extra_bytes(int32_t V, int32_t dim, int64_t n_docs);
 int run_train_sync(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
                    const float *alpha_tab, int64_t blk0, unsigned long long *tstats, hipStream_t s);
+int run_probe_rows(float *matrix, int64_t rows, int32_t cols, int32_t row_stride, int32_t mode, int32_t workgroups,
+                   int32_t iters, float *ms_host, hipStream_t s);
 size_t loglik_extra_bytes(int64_t n_docs);
 int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
                double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, hipStream_t s);
@@ -374,4 +376,16 @@ int w2v_keep_thresholds(const int64_t *vocab_counts, int32_t V, double sample, i
     return launch_thresholds(vocab_counts, V, sample, train_words, thr, as_stream(hip_stream));
 }
 
+int w2v_probe_rows(float *matrix, int64_t rows, int32_t cols, int32_t row_stride, int32_t mode, int32_t workgroups,
+                   int32_t iters, float *ms_host, void *hip_stream) {
+    g_err.clear();
+    if (!matrix || !ms_host) return fail(W2V_E_ARG, "matrix/ms_host is NULL");
+    if (rows < 1 || cols < 1 || row_stride < cols || cols > 1024)
+        return fail(W2V_E_ARG, "need rows >= 1 and 1 <= cols <= min(row_stride, 1024)");
+    if (mode < 0 || mode > 3) return fail(W2V_E_ARG, "mode must be in 0..3");
+    if (workgroups < 1 || iters < 1) return fail(W2V_E_ARG, "workgroups and iters must be >= 1");
+    return run_probe_rows(matrix, rows, cols, row_stride, mode, workgroups, iters, ms_host, as_stream(hip_stream));
+}
+
 }  // extern "C"
+

@@ -144,3 +144,19 @@ def test_binding_refuses_host_tensors(w2v):
     import torch
     with pytest.raises(ValueError):
         w2v.build_vocab(torch.zeros(10, dtype=torch.int32), 10)
+
+
+@pytest.mark.parametrize("args,msg", [
+    ((0, 10, 4, 4, 0, 1, 1), "NULL"),
+    ((0x1000, 0, 4, 4, 0, 1, 1), "rows"),
+    ((0x1000, 10, 5, 4, 0, 1, 1), "cols"),
+    ((0x1000, 10, 4, 4, 4, 1, 1), "mode"),
+    ((0x1000, 10, 4, 4, 0, 0, 1), "workgroups"),
+])
+def test_probe_argument_errors(w2v, args, msg):
+    ms = ctypes.c_float(0.0)
+    m, rows, cols, stride, mode, wg, it = args
+    rc = w2v.lib().w2v_probe_rows(ctypes.c_void_p(m) if m else None, rows, cols, stride, mode, wg, it,
+                                  ctypes.byref(ms), None)
+    assert rc == w2v.W2V_E_ARG
+    assert msg in w2v.last_error()

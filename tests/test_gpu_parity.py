@@ -357,3 +357,29 @@ def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw):
     ref = gold["mean_ll"]
     log(f"  gpu {g:.6f} oracle {ref:.6f} init {gold['init_mean_ll']:.6f}")
     assert abs(g - ref) <= 0.01 * abs(ref)
+
+
+# ------------------------------------------------------------- memory probe
+def test_probe_rows_read_modify_write_counts(w2v, torch_mod):
+    torch = torch_mod
+    # 1 workgroup = 12 wavefronts x 4 rows x iters visits, each adding 1 to the first cols floats of a row;
+    # the adds are plain read-modify-writes, so two visits of one row at the same time may count once
+    m = torch.zeros(1000, 320, dtype=torch.float32, device="cuda")
+    ms = w2v.probe_rows(m, 300, mode=1, workgroups=1, iters=3)
+    assert ms > 0
+    h = m.cpu().numpy()
+    assert h[:, 300:].sum() == 0
+    assert np.all(h == np.round(h)) and h.min() >= 0
+    visits = 12 * 4 * 3
+    assert 0.8 * visits * 300 <= h.sum() <= visits * 300
+    ms = w2v.probe_rows(m, 300, mode=0, workgroups=2, iters=2)
+    assert ms > 0 and m.cpu().numpy().sum() == h.sum()   # reads leave the matrix alone
+    ms = w2v.probe_rows(m, 300, mode=2, workgroups=2, iters=100)
+    assert ms > 0 and m.cpu().numpy().sum() == h.sum()
+    # streaming write: 2 workgroups x 12 wavefronts x 4 rows x 11 rounds cover rows 0..1055, clipped to 1000;
+    # round i writes the value i
+    m.zero_()
+    w2v.probe_rows(m, 320, mode=3, workgroups=2, iters=11)
+    h = m.cpu().numpy()
+    rows = np.arange(1000)
+    assert np.array_equal(h, np.repeat(((rows // 4) % 11).astype(np.float32)[:, None], 320, axis=1))
