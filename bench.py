@@ -46,6 +46,11 @@ def parse():
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
     ap.add_argument("--no-probe", action="store_true", help="skip the random-row memory probe")
+    ap.add_argument("--sweep-cache", action="store_true",
+                    help="instead of the benchmark line: one JSON line per (cache_k, flush_every) of the "
+                         "cache-size x write-back-interval grid (epoch kernel time and held-out log-likelihood)")
+    ap.add_argument("--sweep-k", default="0,1,3,7,15,31,63")
+    ap.add_argument("--sweep-f", default="1,10,100,1000")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first write, then read, 1.28 GB of rows once each (reference dispatches for HBM byte counters)")
     return ap.parse_args()
@@ -110,6 +115,10 @@ def main():
     held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
     ws = torch.empty(w2v.train_workspace_bytes(model, w.n_tokens, p), dtype=torch.uint8, device=dev)
     stats = torch.zeros(w2v.N_STATS, dtype=torch.int64, device=dev)
+
+    if args.sweep_cache:
+        sweep_cache(args, torch, w2v, synth, w, voc, tree, model, held, pe, ws, stats)
+        return
 
     calib = None
     if args.copy_calibration:
@@ -218,6 +227,35 @@ def main():
         "launch": {"workgroups": n_groups, "wavefronts": n_waves},
     }
     print(json.dumps(line), flush=True)
+
+
+def sweep_cache(args, torch, w2v, synth, w, voc, tree, model, held, pe, ws, stats):
+    """Cache size k x write-back interval F (centres per workgroup): the GPU form of the paper's
+    study of the number of cached nodes and of the update interval. Every point starts from the same
+    initial model and trains one epoch with the default write policies; k = 0 has no cache, so one F."""
+    syn0, syn1 = synth.init_weights(voc.V, w.dim)
+    s0 = torch.from_numpy(syn0).to(model.syn0.device)
+    s1 = torch.from_numpy(syn1).to(model.syn0.device)
+    del syn0, syn1
+    for k in (int(x) for x in args.sweep_k.split(",")):
+        for f in ((1,) if k == 0 else tuple(int(x) for x in args.sweep_f.split(","))):
+            model.syn0.zero_()
+            model.syn1.zero_()
+            model.syn0[:, :w.dim].copy_(s0)
+            model.syn1[:voc.V - 1, :w.dim].copy_(s1)
+            p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, arch=w.arch, corpus_tokens=w.n_tokens,
+                           seed=synth.SEED_TRAIN, cache_k=k, flush_every=f, flush_policy=args.flush_policy,
+                           write_policy=args.write_policy, workers=args.workers)
+            w2v.train_hs_epoch(model, voc.tokens, p, stats=stats, workspace=ws)
+            kms = w2v.last_train_kernel_ms()
+            s, npairs, _ = w2v.hs_loglik(model, held, pe)
+            st = stats.cpu().numpy()
+            line = {"sweep": "cache_k x flush_every", "workload": args.workload, "cache_k": k, "flush_every": f,
+                    "flush_policy": args.flush_policy, "write_policy": args.write_policy,
+                    "train_kernel_ms": kms, "words_per_s": int(st[1]) / (kms / 1e3),
+                    "pair_node_updates_per_s": int(st[4]) / (kms / 1e3), "heldout_mean_ll": s / npairs}
+            log(f"k={k} F={f}: {kms:.0f} ms, LL {s / npairs:.5f}")
+            print(json.dumps(line), flush=True)
 
 
 def memory_probe(torch, w2v, rows, cols, stride, dev):

@@ -117,7 +117,10 @@ typedef struct {
 } w2v_model;
 
 typedef struct {
-    int32_t arch;            /* 0 = skip-gram (Algorithm 1), 1 = CBOW (mean of the window as input) */
+    int32_t arch;            /* 0 = skip-gram (Algorithm 1), 1 = CBOW (mean of the window as input),
+                                2 = skip-gram with the reversed orientation: for each window word w in order
+                                the path of w is walked with the centre's vector as input, which gains that
+                                pair's hidden-layer gradient before the next pair (asynchronous mode only) */
     int32_t mode;            /* 0 = asynchronous (lock-free, top-k cache in LDS), 1 = synchronous batches */
     int32_t window;          /* W ("windowsize", §4.1), 1..10; effective half-width uniform on 1..W */
     int32_t doc_len;         /* documents of doc_len raw tokens (1..65535); windows never cross them */

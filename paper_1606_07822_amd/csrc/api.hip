@@ -108,7 +108,8 @@ int check_params(const w2v_params *p, bool training) {
     if (p->first_raw_index < 0 || p->first_raw_index % p->doc_len != 0)
         return fail(W2V_E_ARG, "first_raw_index must be a non-negative multiple of doc_len");
     if (training) {
-        if (p->arch != 0 && p->arch != 1) return fail(W2V_E_ARG, "arch must be 0 (skip-gram) or 1 (CBOW)");
+        if (p->arch < 0 || p->arch > 2)
+            return fail(W2V_E_ARG, "arch must be 0 (skip-gram), 1 (CBOW) or 2 (skip-gram, reversed orientation)");
         if (p->mode != 0 && p->mode != 1) return fail(W2V_E_ARG, "mode must be 0 (async) or 1 (sync)");
         if (p->mode == 1 && p->arch != 0) return fail(W2V_E_ARG, "synchronous mode is skip-gram only");
         if (p->n_epochs < 1 || p->epoch < 0 || p->epoch >= p->n_epochs)

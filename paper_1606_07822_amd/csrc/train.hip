@@ -342,7 +342,8 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
     }
 }
 
-// ARCH 0: skip-gram, window words in groups of PG; ARCH 1: CBOW (one input, the mean).
+// ARCH 0: skip-gram, window words in groups of PG; ARCH 1: CBOW (one input, the mean); ARCH 2: skip-gram
+// with the reversed orientation (the window word's path, the centre's vector as input).
 template <int NE, int PG, int ARCH, int WPB, int PF>
 __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     const int LS = lds_stride<NE>(a.dim);
@@ -393,8 +394,8 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                         const int c = lo + lane + ((lo + lane >= j) ? 1 : 0);
                         wv = kv[c];
                     }
-                    const int len = a.codelen[v];
-                    const uint64_t code = a.code[v];
+                    const int len = ARCH == 2 ? 0 : a.codelen[v];
+                    const uint64_t code = ARCH == 2 ? 0 : a.code[v];
                     const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
 
                     if constexpr (ARCH == 0) {
@@ -459,6 +460,35 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                             }
                         }
                         n_nodes += static_cast<uint64_t>(P) * len;
+                    } else if constexpr (ARCH == 2) {
+                        // reversed orientation: for each window word w in order, the path of w is walked with
+                        // the centre's vector as input, which then gains that pair's hidden-layer gradient
+                        // before the next pair (pair-major, as Algorithm 1 with the roles of v and w swapped)
+                        float x[1][NE], e[1][NE], x0[NE];
+                        float *xr = a.syn0 + static_cast<int64_t>(v) * a.stride;
+                        load_row<NE>(x[0], xr, lane, a.dim);
+#pragma unroll
+                        for (int i = 0; i < NE; ++i) x0[i] = x[0][i];
+                        int nodes = 0;
+                        for (int q = 0; q < P; ++q) {
+                            const int w = __builtin_amdgcn_readlane(wv, q);
+                            const int lw = a.codelen[w];
+                            const uint64_t cw = a.code[w];
+                            const int pw = (lane < lw) ? a.points[a.point_off[w] + lane] : 0;
+                            zero_row<NE>(e[0]);
+                            walk_path<NE, 1, PF>(a, val, x, e, 1, pw, lw, cw, alpha, lane);
+#pragma unroll
+                            for (int i = 0; i < NE; ++i) x[0][i] += e[0][i];
+                            nodes += lw;
+                        }
+                        if (a.write_policy & 2) {
+                            store_row<NE>(xr, x[0], lane, a.dim, a.full_rows);
+                        } else {
+#pragma unroll
+                            for (int i = 0; i < NE; ++i) x0[i] = x[0][i] - x0[i];
+                            atomic_add_row<NE>(xr, x0, lane, a.dim, a.full_rows);
+                        }
+                        n_nodes += nodes;
                     } else {
                         // CBOW: h = mean of the window vectors; one path walk; e added to each window vector
                         float h[1][NE], e[1][NE];
@@ -533,6 +563,7 @@ struct Variant {
 template <int NE, int PG, int WPB, int PF>
 Variant variant(int arch) {
     if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE, PG, lds_stride<NE>};
+    if (arch == 2) return Variant{k_train<NE, 1, 2, WPB, PF>, WPB, NE, 1, lds_stride<NE>};
     return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE, 1, lds_stride<NE>};
 }
 

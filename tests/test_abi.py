@@ -106,7 +106,8 @@ def _params(w2v, **kw):
     ({}, dict(doc_len=0), "doc_len"),
     ({}, dict(sample=1.5), "sample"),
     ({}, dict(first_raw_index=7), "first_raw_index"),
-    ({}, dict(arch=2), "arch"),
+    ({}, dict(arch=3), "arch"),
+    ({}, dict(mode=1, arch=2), "synchronous"),
     ({}, dict(mode=1, arch=1), "synchronous"),
     ({}, dict(epoch=1, n_epochs=1), "epoch"),
     ({}, dict(flush_every=0), "flush_every"),

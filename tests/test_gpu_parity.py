@@ -383,3 +383,76 @@ def test_probe_rows_read_modify_write_counts(w2v, torch_mod):
     h = m.cpu().numpy()
     rows = np.arange(1000)
     assert np.array_equal(h, np.repeat(((rows // 4) % 11).astype(np.float32)[:, None], 320, axis=1))
+
+
+# ------------------------------------------------------------- reversed orientation, several epochs
+# arch 2: each window word's path is walked with the centre's vector as input, which takes each pair's
+# gradient before the next pair -- the oracle's pair-major order with the orientation flag, exactly.
+@pytest.mark.parametrize("k,dim,wp,win", [(0, 100, 1, 5), (31, 100, 1, 5), (31, 300, 5, 5), (31, 300, 0, 5),
+                                          (7, 200, 5, 10), (31, 600, 5, 3)])
+def test_single_worker_reversed_orientation(w2v, k, dim, wp, win):
+    log(f"single worker reversed k={k} dim={dim} write_policy={wp} window={win}")
+    s = oracle_side("sg_v30k_d100")
+    voc, tree = gpu_side(w2v, s)
+    tv = s.tv[:3000]
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, dim, window=win, sample=1e-3, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, cache_k=k, flush_every=10, order=0, orient=1)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=win, sample=1e-3, corpus_tokens=s.tv.size, cache_k=k, flush_every=10, workers=1, arch=2,
+                   write_policy=wp)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4
+    assert row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+# Later epochs draw other subsamples and windows (Philox counter) and continue the learning-rate decay.
+@pytest.mark.parametrize("arch", [0, 2])
+def test_single_worker_second_epoch(w2v, arch):
+    s = oracle_side("sg_v30k_d100")
+    voc, tree = gpu_side(w2v, s)
+    tv = s.tv[:3000]
+    syn0, syn1 = synth.init_weights(s.voc.V, 100, syn1_scale=0.005)
+    a0, a1 = syn0.copy(), syn1.copy()
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    for e in range(2):
+        op = oracle.params(s.voc.V, 100, window=5, sample=1e-3, train_words=s.voc.train_words, corpus_tokens=tv.size,
+                           cache_k=31, flush_every=10, order=1 if arch == 0 else 0, orient=1 if arch == 2 else 0,
+                           epoch=e, n_epochs=2)
+        ost = oracle.train(a0, a1, s.tree, tv, op)
+        p = w2v.Params(window=5, sample=1e-3, corpus_tokens=tv.size, cache_k=31, flush_every=10, workers=1,
+                       arch=arch, epoch=e, n_epochs=2)
+        st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+        assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4
+    assert row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+@pytest.mark.parametrize("name,gold,arch,epochs", [
+    ("sg_v30k_d100", "sg_v30k_d100_orient1", 2, 1),
+    ("sg_v30k_d100", "sg_v30k_d100_epochs3", 0, 3),
+])
+def test_async_loglik_reversed_and_epochs(w2v, name, gold, arch, epochs):
+    log(f"async LL {gold}")
+    g = golden(gold)
+    s = oracle_side(name)
+    assert s.voc.V == g["V"] and s.voc.train_words == g["train_words"]
+    voc, tree = gpu_side(w2v, s)
+    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    for e in range(epochs):
+        p = w2v.Params(window=s.w.window, sample=s.w.sample, corpus_tokens=s.tv.size, arch=arch, alpha0=s.w.alpha0,
+                       epoch=e, n_epochs=epochs)
+        st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
+        assert list(st) == (g["stats"][e] if epochs > 1 else g["stats"])
+    held = corpus(name, heldout=True)
+    hv = to_dev(oracle.remap(held, s.voc.id_to_vocab))
+    sg, npairs, _ = w2v.hs_loglik(model, hv, w2v.Params(window=s.w.window, sample=s.w.sample, seed=synth.SEED_EVAL))
+    assert npairs == g["heldout_pairs"]
+    log(f"  gpu {sg / npairs:.6f} oracle {g['mean_ll']:.6f} init {g['init_mean_ll']:.6f}")
+    assert abs(sg / npairs - g["mean_ll"]) <= 0.01 * abs(g["mean_ll"])

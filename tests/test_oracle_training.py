@@ -10,7 +10,10 @@ What fixes these other than the oracle itself:
   * the cache of Algorithm 1 with one worker changes nothing beyond the
     rounding of its flush (invariant of the caching scheme, §3.2);
   * swapping the window and node loops is exact when a window holds no
-    repeated word (invariant).
+    repeated word (invariant);
+  * with the reversed orientation, a centre's pairs are gradient steps of
+    log P(w|v) taken one after the other, each at the model the previous one
+    left (finite differences).
 """
 import math
 
@@ -102,6 +105,38 @@ def test_skipgram_pair_update_is_alpha_times_gradient(V, dim, seed, order):
             np.testing.assert_allclose(a1[n] - syn1[n], alpha * gy, rtol=2e-4, atol=2e-8)
         else:
             np.testing.assert_array_equal(a1[n], syn1[n])
+
+
+@pytest.mark.parametrize("V,dim,seed", [(6, 4, 0), (13, 5, 1), (20, 8, 2)])
+def test_reversed_orientation_pairs_are_sequential_gradient_steps(V, dim, seed):
+    tree, syn0, syn1 = small_model(V, dim, seed)
+    v, w1, w2 = 2, V - 1, 1
+    tok = np.array([v, w1, w2], np.int32)
+    alpha = 0.025
+    # a sampler seed whose first centre (v) takes both neighbours: half-width 2
+    for s in range(200):
+        p = oracle.params(V, dim, window=2, alpha0=alpha, corpus_tokens=3, max_centres=1, orient=1, seed=s)
+        pr = oracle.sample_pairs(tok, p, tree.vocab_counts)
+        if list(pr.centre[:2]) == [0, 0] and list(pr.context[:2]) == [1, 2]:
+            break
+    else:
+        pytest.fail("no seed gives the first centre a half-width of 2")
+    a0, a1 = syn0.copy(), syn1.copy()
+    st = oracle.train(a0, a1, tree, tok, p)
+    assert st[3] == 2 and st[4] == int(tree.codelen[w1]) + int(tree.codelen[w2])
+    x = syn0[v].astype(np.float64)
+    y = syn1.astype(np.float64)
+    for w in (w1, w2):                   # each pair at the state the previous one left
+        gx = fd_grad_x(x, y, tree, w)
+        pts, _ = tree.path(w)
+        gy = {n: fd_grad_y(x, y, tree, w, n) for n in pts}
+        x = x + alpha * gx
+        for n in pts:
+            y[n] = y[n] + alpha * gy[n]
+    np.testing.assert_allclose(a0[v], x, rtol=2e-4, atol=2e-8)
+    np.testing.assert_allclose(a1, y, rtol=2e-4, atol=2e-8)
+    others = [r for r in range(V) if r != v]
+    np.testing.assert_array_equal(a0[others], syn0[others])
 
 
 def test_one_step_from_zero_syn1_closed_form():
