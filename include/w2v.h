@@ -144,7 +144,9 @@ typedef struct {
     int32_t hot_k;           /* with write_policy bit 0: the hot_k inner nodes created just before the cached
                                 ones (on most paths, so the most contended rows) still take atomic adds of
                                 their change; >= 0 */
-    int32_t reserved2[5];
+    int32_t negative;        /* negative sampling (w2v_train_ns_epoch, w2v_ns_objective): negatives per centre,
+                                shared by its window words; 1..11 (1..7 above 320 columns); ignored elsewhere */
+    int32_t reserved2[4];
 } w2v_params;
 
 /* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,
@@ -210,6 +212,59 @@ int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, c
                   size_t workspace_bytes, void *hip_stream);
 
 /* ------------------------------------------------------------------------
+ * Negative sampling: the alternative objective to the hierarchical softmax
+ * that §2 names, trained in the mini-batch form of Ji et al. that the opening
+ * of §3.2 describes (every window word of a centre trains against the same
+ * targets, all gradients of the centre taken before any of its updates).
+ * For these calls m->syn1 holds the output vectors of the words,
+ * float[V][row_stride]; the Huffman arrays of m are not used (may be NULL).
+ *
+ * w2v_build_noise_table: the noise distribution, unigram counts raised to
+ * 3/4, with the weight of count c taken in integers as isqrt(c * isqrt(c)),
+ * laid out in table int32[2^log2_size]: entry i holds the vocabulary index
+ * v with Q[v] <= floor(i Q / 2^log2_size) < Q[v+1] (Q[v] = weight of the
+ * indices below v, Q = total). log2_size in 1..30; total_weight_host gets Q.
+ * Errors: W2V_E_ARG for bad sizes or NULL pointers; W2V_E_RANGE if Q is not
+ * in [1, 2^(63 - log2_size)). Synchronises the stream.
+ * ---------------------------------------------------------------------- */
+size_t w2v_noise_table_workspace_bytes(int32_t V);
+int w2v_build_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, int32_t *table,
+                          int64_t *total_weight_host, void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/* ------------------------------------------------------------------------
+ * One pass of skip-gram with shared negatives over tokens (vocabulary
+ * indices, -1 = dropped): the same subsampling, documents, window draws and
+ * learning-rate schedule as w2v_train_hs_epoch. Per kept centre v with
+ * window words w_1..w_P, its targets are v (label 1) and p->negative
+ * negatives (label 0): negative 4h+i is table[r_i >> (32 - log2_size)], r =
+ * Philox4x32-10(counter (raw index lo, raw index hi, epoch, 1 + h), key =
+ * seed); one equal to v is dropped. With S_qk = syn0[w_q] . syn1[t_k] and
+ * g_qk = alpha (label_k - sigmoid(S_qk)), syn0[w_q] gains sum_k g_qk
+ * syn1[t_k] and syn1[t_k] gains sum_q g_qk syn0[w_q], all from the values
+ * before the centre. Rows are changed with atomic adds; centres run
+ * concurrently (lock-free), so results vary with scheduling except with
+ * workers = 1. stats int64[W2V_N_STATS]: raw tokens, in-vocabulary tokens,
+ * kept centres, pairs, pair-target updates. Asynchronous (mode 0) skip-gram
+ * only; dim <= 512. Errors as w2v_train_hs_epoch, and W2V_E_ARG for a NULL
+ * table, log2_size outside 1..30 or negative out of range.
+ * ---------------------------------------------------------------------- */
+size_t w2v_train_ns_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
+int w2v_train_ns_epoch(const w2v_model *m, const int32_t *noise_table, int32_t log2_size, const int32_t *tokens,
+                       int64_t n_tokens, const w2v_params *p, int64_t *stats, void *workspace, size_t workspace_bytes,
+                       void *hip_stream);
+
+/* Negative-sampling objective (evaluation) over the sampler's pairs drawn
+   with p's seed and epoch, each pair with its centre's negatives: sum_host =
+   sum over pairs (v, w) of log sigmoid(syn0[w] . syn1[v]) + sum over kept
+   negatives n of log sigmoid(-syn0[w] . syn1[n]). Dot products in fp32, logs
+   and sums in fp64, in a fixed order (deterministic). n_terms_host (may be
+   NULL) = number of log-sigmoid terms. Read-only. Synchronises the stream. */
+size_t w2v_ns_objective_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
+int w2v_ns_objective(const w2v_model *m, const int32_t *noise_table, int32_t log2_size, const int32_t *tokens,
+                     int64_t n_tokens, const w2v_params *p, double *sum_host, int64_t *n_pairs_host,
+                     int64_t *n_terms_host, void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/* ------------------------------------------------------------------------
  * Test hooks (not part of the training contract).
  *
  * w2v_sample_pairs: the (centre, context) pairs of the sampler in stream
@@ -221,6 +276,12 @@ int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, c
  *
  * w2v_keep_thresholds: thr[v] = 2^32 if the keep probability is >= 1, else
  * floor(p_keep 2^32); a token is kept iff its first Philox word < thr.
+ *
+ * w2v_sample_negatives: the p->negative negatives of every kept centre in
+ * stream order (-1 where dropped), the first negatives_cap centres written to
+ * negatives int32[cap][negative] (may be NULL); checksum_host = sum over kept
+ * centres and k of fmix64(raw * 0x9E3779B97F4A7C15 + k * 2^32 + (negative + 1))
+ * mod 2^64. Synchronises the stream.
  * ---------------------------------------------------------------------- */
 size_t w2v_sample_pairs_workspace_bytes(int32_t V, int64_t n_tokens, const w2v_params *p);
 int w2v_sample_pairs(const int32_t *tokens, int64_t n_tokens, int32_t V, const int64_t *vocab_counts,
@@ -229,6 +290,11 @@ int w2v_sample_pairs(const int32_t *tokens, int64_t n_tokens, int32_t V, const i
                      uint64_t *checksum_host, void *workspace, size_t workspace_bytes, void *hip_stream);
 int w2v_keep_thresholds(const int64_t *vocab_counts, int32_t V, double sample, int64_t train_words, uint64_t *thr,
                         void *hip_stream);
+size_t w2v_sample_negatives_workspace_bytes(int32_t V, int64_t n_tokens, const w2v_params *p);
+int w2v_sample_negatives(const int32_t *tokens, int64_t n_tokens, int32_t V, const int64_t *vocab_counts,
+                         int64_t train_words, const w2v_params *p, const int32_t *noise_table, int32_t log2_size,
+                         int32_t *negatives, int64_t negatives_cap, int64_t *n_kept_host, uint64_t *checksum_host,
+                         void *workspace, size_t workspace_bytes, void *hip_stream);
 
 /* ------------------------------------------------------------------------
  * Measurement utility (not part of the method): the practical memory ceiling

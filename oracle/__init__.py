@@ -7,7 +7,9 @@ Python binding never do.
 Every function follows Vuurens, Eickhoff and de Vries, "Efficient Parallel
 Learning of Word2Vec": Algorithm 1 (Cached Skipgram HS) for training, §2 for
 the hierarchical softmax over a binary Huffman tree, §4.1 for the settings
-(mintf, windowsize, vectorsize, downsample). The readings used where the paper
+(mintf, windowsize, vectorsize, downsample). Negative sampling, named in §2
+as the alternative objective, follows Ji et al.'s shared-negative mini-batch
+as the opening of §3.2 describes it. The readings used where the paper
 is silent are listed at the top of ``w2v_oracle.c``.
 
 Parity pins (what fixes the oracle other than itself) live in
@@ -37,7 +39,7 @@ class Params(ctypes.Structure):
                 ("alpha0", F32), ("epoch", I32), ("n_epochs", I32), ("train_words", I64),
                 ("corpus_tokens", I64), ("first_raw_index", I64), ("seed", U64), ("cache_k", I32),
                 ("flush_every", I32), ("order", I32), ("orient", I32), ("arch", I32), ("sync_batch", I32),
-                ("max_centres", I64)]
+                ("max_centres", I64), ("negative", I32), ("reserved", I32)]
 
 
 class _Tree(ctypes.Structure):
@@ -90,6 +92,16 @@ def lib():
         L.or_log_prob_f64.argtypes = [P, P, I32, ctypes.POINTER(_Tree), I32]
         L.or_loglik.restype = ctypes.c_int
         L.or_loglik.argtypes = [P, P, ctypes.POINTER(_Tree), P, I64, ctypes.POINTER(Params), P, P, P]
+        L.or_noise_weights.restype = I64
+        L.or_noise_weights.argtypes = [P, I32, P]
+        L.or_noise_table.restype = ctypes.c_int
+        L.or_noise_table.argtypes = [P, I32, I32, P]
+        L.or_sample_negatives.restype = I64
+        L.or_sample_negatives.argtypes = [P, I64, ctypes.POINTER(Params), P, P, I32, P, I64, P, P]
+        L.or_train_ns.restype = ctypes.c_int
+        L.or_train_ns.argtypes = [P, P, P, P, I32, P, I64, ctypes.POINTER(Params), P]
+        L.or_ns_objective.restype = ctypes.c_int
+        L.or_ns_objective.argtypes = [P, P, P, P, I32, P, I64, ctypes.POINTER(Params), P, P, P]
         _LIB = L
     return _LIB
 
@@ -202,9 +214,10 @@ def alpha(alpha0: float, raw_pos: int, epoch: int, n_epochs: int, corpus_tokens:
 def params(V: int, dim: int, *, window: int, sample: float = 0.0, alpha0: float = 0.025, train_words: int = 0,
            corpus_tokens: int = 0, seed: int = 3, epoch: int = 0, n_epochs: int = 1, doc_len: int = 1000,
            first_raw_index: int = 0, cache_k: int = 0, flush_every: int = 10, order: int = 0, orient: int = 0,
-           arch: int = 0, sync_batch: int = 4096, max_centres: int = -1) -> Params:
+           arch: int = 0, sync_batch: int = 4096, max_centres: int = -1, negative: int = 5) -> Params:
     return Params(V, dim, window, doc_len, sample, alpha0, epoch, n_epochs, train_words, corpus_tokens,
-                  first_raw_index, seed, cache_k, flush_every, order, orient, arch, sync_batch, max_centres)
+                  first_raw_index, seed, cache_k, flush_every, order, orient, arch, sync_batch, max_centres, negative,
+                  0)
 
 
 @dataclass
@@ -283,3 +296,68 @@ def loglik(syn0: np.ndarray, syn1: np.ndarray, tree: Tree, tokens_v: np.ndarray,
                        ctypes.byref(s), ctypes.byref(npairs), ctypes.byref(nn)):
         raise RuntimeError("or_loglik failed")
     return float(s.value), int(npairs.value), int(nn.value)
+
+
+# ---------------------------------------------------------- negative sampling
+def noise_weights(vocab_counts: np.ndarray):
+    """(weights int64[V], total): isqrt(c * isqrt(c)) per word (unigram^(3/4) in integers)."""
+    vc = np.ascontiguousarray(vocab_counts, dtype=np.int64)
+    w = np.empty(vc.size, np.int64)
+    tot = lib().or_noise_weights(_ptr(vc), vc.size, _ptr(w))
+    return w, int(tot)
+
+
+def noise_table(vocab_counts: np.ndarray, log2_size: int) -> np.ndarray:
+    vc = np.ascontiguousarray(vocab_counts, dtype=np.int64)
+    t = np.empty(1 << log2_size, np.int32)
+    if lib().or_noise_table(_ptr(vc), vc.size, log2_size, _ptr(t)) != 0:
+        raise ValueError("bad noise-table input")
+    return t
+
+
+@dataclass
+class Negatives:
+    negatives: np.ndarray   # int32[min(cap, kept)][K], -1 = dropped (equal to the centre)
+    n_kept: int
+    checksum: int
+
+
+def sample_negatives(tokens_v: np.ndarray, p: Params, vocab_counts: np.ndarray, table: np.ndarray, log2_size: int,
+                     cap: int = 0) -> Negatives:
+    tok = np.ascontiguousarray(tokens_v, dtype=np.int32)
+    vc = np.ascontiguousarray(vocab_counts, dtype=np.int64)
+    out = np.empty((max(cap, 0), p.negative), np.int32)
+    nk = ctypes.c_int64(0)
+    cs = ctypes.c_uint64(0)
+    r = lib().or_sample_negatives(_ptr(tok), tok.size, ctypes.byref(p), _ptr(vc), _ptr(table), log2_size,
+                                  _ptr(out) if cap > 0 else None, cap, ctypes.byref(nk), ctypes.byref(cs))
+    if r < 0:
+        raise RuntimeError("or_sample_negatives failed")
+    return Negatives(out[:min(cap, int(nk.value))], int(nk.value), int(cs.value))
+
+
+def train_ns(syn0: np.ndarray, syn1: np.ndarray, vocab_counts: np.ndarray, table: np.ndarray, log2_size: int,
+             tokens_v: np.ndarray, p: Params) -> np.ndarray:
+    """Skip-gram with shared negatives, in place on syn0 [V,d] / syn1 [V,d]. Returns stats int64[5]."""
+    assert syn0.dtype == np.float32 and syn1.dtype == np.float32 and syn1.shape[0] == syn0.shape[0]
+    tok = np.ascontiguousarray(tokens_v, dtype=np.int32)
+    vc = np.ascontiguousarray(vocab_counts, dtype=np.int64)
+    st = np.zeros(5, np.int64)
+    if lib().or_train_ns(_ptr(syn0), _ptr(syn1), _ptr(vc), _ptr(table), log2_size, _ptr(tok), tok.size,
+                         ctypes.byref(p), _ptr(st)):
+        raise RuntimeError("or_train_ns failed")
+    return st
+
+
+def ns_objective(syn0: np.ndarray, syn1: np.ndarray, vocab_counts: np.ndarray, table: np.ndarray, log2_size: int,
+                 tokens_v: np.ndarray, p: Params):
+    """(sum over the sampler's pairs of the negative-sampling objective, n_pairs, n_terms)."""
+    tok = np.ascontiguousarray(tokens_v, dtype=np.int32)
+    vc = np.ascontiguousarray(vocab_counts, dtype=np.int64)
+    s = ctypes.c_double(0)
+    npairs = ctypes.c_int64(0)
+    nt = ctypes.c_int64(0)
+    if lib().or_ns_objective(_ptr(syn0), _ptr(syn1), _ptr(vc), _ptr(table), log2_size, _ptr(tok), tok.size,
+                             ctypes.byref(p), ctypes.byref(s), ctypes.byref(npairs), ctypes.byref(nt)):
+        raise RuntimeError("or_ns_objective failed")
+    return float(s.value), int(npairs.value), int(nt.value)

@@ -34,6 +34,25 @@
  *   R12 window: effective half-width W - b with b uniform on {0..W-1}.
  *   R13 documents of doc_len raw tokens; windows never cross them; dropped and
  *       subsampled tokens are removed before windowing.
+ *
+ * Negative sampling (named in §2 as the alternative to the hierarchical
+ * softmax; the opening of §3.2 describes Ji et al.'s mini-batch form of it):
+ *   N1  the noise distribution is the unigram distribution raised to 3/4 (the
+ *       choice of Mikolov et al., whom §2 cites), with the weight of a word of
+ *       count c taken in integers as isqrt(c * isqrt(c)), so that every
+ *       implementation draws the same words.
+ *   N2  noise table of T = 2^L entries: entry i holds the word v whose weight
+ *       prefix sums satisfy Q[v] <= floor(i Q / T) < Q[v+1]; a draw r (32 bits)
+ *       picks entry r >> (32 - L).
+ *   N3  a centre's K negatives are shared by all of its window words (Ji et
+ *       al., §3.2): negative 4h+i is drawn from word i of Philox4x32-10 with
+ *       counter (raw index lo, hi, epoch, 1 + h); a negative equal to the centre
+ *       word is dropped.
+ *   N4  mini-batch update (§3.2, level-3 BLAS form; §4.3 notes that it does
+ *       not use updated vectors within a mini-batch): with X the window words' vectors and Y
+ *       the output vectors of the centre (label 1) and its negatives (label 0),
+ *       S = X Y^T, G = alpha (labels - sigmoid(S)); X gains G Y and Y gains
+ *       G^T X, both from the values at the start of the centre.
  */
 #include "w2v_oracle.h"
 
@@ -651,6 +670,224 @@ int or_loglik(const float *syn0, const float *syn1, const or_tree *t, const int3
     *sum_ll = s;
     *n_pairs = np;
     if (n_nodes) *n_nodes = nn;
+    doc_free(&d);
+    free(thr);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Negative sampling: noise table (N1, N2), shared negatives (N3), mini-batch */
+/* updates (N4), objective.                                                   */
+/* ------------------------------------------------------------------------ */
+
+/* floor(sqrt(x)) for x < 2^62, by bisection on integers. */
+static uint64_t isqrt_u64(uint64_t x) {
+    uint64_t lo = 0, hi = (uint64_t)1 << 31;
+    while (lo < hi) {           /* largest m with m*m <= x */
+        uint64_t mid = (lo + hi + 1) / 2;
+        if (mid * mid <= x) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+/* weight[v] = isqrt(c * isqrt(c)), c = count of v (N1); returns the total. */
+int64_t or_noise_weights(const int64_t *vocab_counts, int32_t V, int64_t *weight) {
+    int64_t tot = 0;
+    for (int32_t v = 0; v < V; v++) {
+        uint64_t c = (uint64_t)vocab_counts[v];
+        weight[v] = (int64_t)isqrt_u64(c * isqrt_u64(c));
+        tot += weight[v];
+    }
+    return tot;
+}
+
+/* table[i] = v with Q[v] <= floor(i * Q / 2^L) < Q[v+1] (N2). Returns -1 on bad input. */
+int or_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, int32_t *table) {
+    if (V < 1 || log2_size < 1 || log2_size > 30) return -1;
+    int64_t *wt = (int64_t *)malloc(sizeof(int64_t) * (size_t)V);
+    if (!wt) return -1;
+    int64_t tot = or_noise_weights(vocab_counts, V, wt);
+    if (tot <= 0 || tot >= ((int64_t)1 << (63 - log2_size))) { free(wt); return -1; }   /* i * Q < 2^63 */
+    int64_t T = (int64_t)1 << log2_size;
+    int32_t v = 0;
+    int64_t q_hi = wt[0];       /* Q[v+1] */
+    for (int64_t i = 0; i < T; i++) {
+        int64_t u = (int64_t)(((uint64_t)i * (uint64_t)tot) >> log2_size);
+        while (u >= q_hi) { v++; q_hi += wt[v]; }
+        table[i] = v;
+    }
+    free(wt);
+    return 0;
+}
+
+/* The K shared negatives of the centre at global raw index raw (N3); -1 where dropped. */
+static void draw_negatives(uint64_t seed, int64_t raw, int32_t epoch, int32_t K, const int32_t *table,
+                           int32_t log2_size, int32_t centre, int32_t *neg) {
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    for (int32_t h = 0; 4 * h < K; h++) {
+        uint32_t ctr[4] = {(uint32_t)raw, (uint32_t)((uint64_t)raw >> 32), (uint32_t)epoch, 1u + (uint32_t)h};
+        uint32_t r[4];
+        or_philox4x32_10(ctr, key, r);
+        for (int32_t i = 0; i < 4 && 4 * h + i < K; i++) {
+            int32_t t = table[r[i] >> (32 - log2_size)];
+            neg[4 * h + i] = (t == centre) ? -1 : t;
+        }
+    }
+}
+
+/*
+ * The negatives of every kept centre in stream order: the first cap centres'
+ * K values go to negatives[cap][K] (may be NULL); checksum = sum over all
+ * kept centres and k of fmix64(raw * 0x9E3779B97F4A7C15 + k * 2^32 + (neg + 1)).
+ * Returns the number of kept centres.
+ */
+int64_t or_sample_negatives(const int32_t *tokens, int64_t n, const or_params *p, const int64_t *vocab_counts,
+                            const int32_t *table, int32_t log2_size, int32_t *negatives, int64_t cap,
+                            int64_t *n_kept, uint64_t *checksum) {
+    if (p->negative < 1 || p->negative > 64) return -1;
+    doc_t d;
+    if (doc_alloc(&d, p->doc_len)) return -1;
+    uint64_t *thr = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)p->V);
+    if (!thr) return -1;
+    or_keep_thresholds(vocab_counts, p->V, p->sample, p->train_words, thr);
+    int32_t neg[64];
+    int64_t nk = 0, inv = 0;
+    uint64_t cs = 0;
+    for (int64_t lo = 0; lo < n; lo += p->doc_len) {
+        doc_sample(tokens, n, p, thr, lo, &d, &inv);
+        for (int32_t j = 0; j < d.n; j++) {
+            draw_negatives(p->seed, d.raw[j], p->epoch, p->negative, table, log2_size, d.vid[j], neg);
+            for (int32_t k = 0; k < p->negative; k++) {
+                if (negatives && nk < cap) negatives[nk * p->negative + k] = neg[k];
+                cs += fmix64((uint64_t)d.raw[j] * 0x9E3779B97F4A7C15ULL + ((uint64_t)k << 32) +
+                             (uint64_t)(int64_t)(neg[k] + 1));
+            }
+            nk++;
+        }
+    }
+    doc_free(&d);
+    free(thr);
+    if (n_kept) *n_kept = nk;
+    if (checksum) *checksum = cs;
+    return nk;
+}
+
+/*
+ * One epoch of skip-gram with shared negatives, one sequential worker (N3,
+ * N4). Per kept centre v with window words w_1..w_m and targets
+ * t_0 = v (label 1), t_1..t_K its negatives (label 0, dropped ones skipped):
+ *   s_qk = vector[w_q] . out[t_k],  g_qk = alpha (label_k - sigmoid(s_qk))
+ *   dx_q = sum_k g_qk out[t_k],     dy_k = sum_q g_qk vector[w_q]
+ * all from the values at the start of the centre; then vector[w_q] += dx_q
+ * (q ascending) and out[t_k] += dy_k (k ascending).
+ * stats: [raw, in-vocabulary, kept centres, pairs, pair-target updates].
+ */
+int or_train_ns(float *syn0, float *syn1, const int64_t *vocab_counts, const int32_t *table, int32_t log2_size,
+                const int32_t *tokens, int64_t n, const or_params *p, int64_t *stats) {
+    const int32_t dim = p->dim, K = p->negative;
+    if (p->V < 2 || p->window < 1 || p->window > 1024 || p->doc_len < 1 || K < 1 || K > 64) return -1;
+    doc_t d;
+    if (doc_alloc(&d, p->doc_len)) return -1;
+    uint64_t *thr = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)p->V);
+    int32_t M = 2 * p->window;
+    float *dx = (float *)malloc(sizeof(float) * (size_t)dim * M);
+    float *dy = (float *)malloc(sizeof(float) * (size_t)dim * (K + 1));
+    float *g = (float *)malloc(sizeof(float) * (size_t)M * (K + 1));
+    int32_t ctx[2 * 1024 + 2], tgt[65];
+    if (!thr || !dx || !dy || !g) return -1;
+    or_keep_thresholds(vocab_counts, p->V, p->sample, p->train_words, thr);
+
+    int64_t raw = 0, inv = 0, kept = 0, pairs = 0, updates = 0;
+    for (int64_t lo = 0; lo < n; lo += p->doc_len) {
+        int64_t hi = lo + p->doc_len < n ? lo + p->doc_len : n;
+        raw += hi - lo;
+        doc_sample(tokens, n, p, thr, lo, &d, &inv);
+        for (int32_t j = 0; j < d.n; j++) {
+            if (p->max_centres >= 0 && kept >= p->max_centres) break;
+            kept++;
+            int32_t m = window_of(&d, j, ctx);
+            if (m == 0) continue;
+            float alpha = or_alpha(p->alpha0, d.raw[j], p->epoch, p->n_epochs, p->corpus_tokens);
+            tgt[0] = d.vid[j];
+            draw_negatives(p->seed, d.raw[j], p->epoch, K, table, log2_size, d.vid[j], tgt + 1);
+            /* gradients at the snapshot */
+            for (int32_t q = 0; q < m; q++) {
+                const float *x = syn0 + (size_t)d.vid[ctx[q]] * dim;
+                for (int32_t k = 0; k <= K; k++) {
+                    if (tgt[k] < 0) { g[q * (K + 1) + k] = 0.0f; continue; }
+                    float f = sigmoidf(sdot(dim, x, syn1 + (size_t)tgt[k] * dim));
+                    g[q * (K + 1) + k] = ((k == 0 ? 1.0f : 0.0f) - f) * alpha;
+                    updates++;
+                }
+            }
+            for (int32_t q = 0; q < m; q++) {
+                float *e = dx + (size_t)q * dim;
+                memset(e, 0, sizeof(float) * (size_t)dim);
+                for (int32_t k = 0; k <= K; k++)
+                    if (tgt[k] >= 0) saxpy(dim, g[q * (K + 1) + k], syn1 + (size_t)tgt[k] * dim, e);
+            }
+            for (int32_t k = 0; k <= K; k++) {
+                float *e = dy + (size_t)k * dim;
+                memset(e, 0, sizeof(float) * (size_t)dim);
+                if (tgt[k] < 0) continue;
+                for (int32_t q = 0; q < m; q++)
+                    saxpy(dim, g[q * (K + 1) + k], syn0 + (size_t)d.vid[ctx[q]] * dim, e);
+            }
+            /* apply */
+            for (int32_t q = 0; q < m; q++) saxpy(dim, 1.0f, dx + (size_t)q * dim, syn0 + (size_t)d.vid[ctx[q]] * dim);
+            for (int32_t k = 0; k <= K; k++)
+                if (tgt[k] >= 0) saxpy(dim, 1.0f, dy + (size_t)k * dim, syn1 + (size_t)tgt[k] * dim);
+            pairs += m;
+        }
+    }
+    if (stats) { stats[0] = raw; stats[1] = inv; stats[2] = kept; stats[3] = pairs; stats[4] = updates; }
+    doc_free(&d);
+    free(thr); free(dx); free(dy); free(g);
+    return 0;
+}
+
+/*
+ * Negative-sampling objective over the sampler's pairs (fp64 sums): for pair
+ * (v, w) with the centre's negatives n_k (drawn with p's seed and epoch),
+ * log sigmoid(x_w . y_v) + sum over kept k of log sigmoid(-x_w . y_{n_k}).
+ */
+int or_ns_objective(const float *syn0, const float *syn1, const int64_t *vocab_counts, const int32_t *table,
+                    int32_t log2_size, const int32_t *tokens, int64_t n, const or_params *p, double *sum,
+                    int64_t *n_pairs, int64_t *n_terms) {
+    const int32_t dim = p->dim, K = p->negative;
+    if (K < 1 || K > 64) return -1;
+    doc_t d;
+    if (doc_alloc(&d, p->doc_len)) return -1;
+    uint64_t *thr = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)p->V);
+    if (!thr) return -1;
+    or_keep_thresholds(vocab_counts, p->V, p->sample, p->train_words, thr);
+    int32_t ctx[2 * 1024 + 2], tgt[65];
+    int64_t inv = 0, np = 0, nt = 0;
+    double s = 0.0;
+    for (int64_t lo = 0; lo < n; lo += p->doc_len) {
+        doc_sample(tokens, n, p, thr, lo, &d, &inv);
+        for (int32_t j = 0; j < d.n; j++) {
+            int32_t m = window_of(&d, j, ctx);
+            if (m == 0) continue;
+            tgt[0] = d.vid[j];
+            draw_negatives(p->seed, d.raw[j], p->epoch, K, table, log2_size, d.vid[j], tgt + 1);
+            for (int32_t q = 0; q < m; q++) {
+                const float *x = syn0 + (size_t)d.vid[ctx[q]] * dim;
+                for (int32_t k = 0; k <= K; k++) {
+                    if (tgt[k] < 0) continue;
+                    const float *y = syn1 + (size_t)tgt[k] * dim;
+                    double z = 0.0;
+                    for (int32_t i = 0; i < dim; i++) z += (double)x[i] * (double)y[i];
+                    s += log_sigmoid(k == 0 ? z : -z);
+                    nt++;
+                }
+                np++;
+            }
+        }
+    }
+    *sum = s;
+    *n_pairs = np;
+    if (n_terms) *n_terms = nt;
     doc_free(&d);
     free(thr);
     return 0;

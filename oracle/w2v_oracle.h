@@ -58,6 +58,8 @@ typedef struct {
     int32_t arch;             /* 0 = skip-gram, 1 = CBOW */
     int32_t sync_batch;       /* synchronous mode: centres per batch */
     int64_t max_centres;      /* stop after this many kept centres (-1 = all) */
+    int32_t negative;         /* negative sampling: negatives shared by a centre's window (N3) */
+    int32_t reserved;
 } or_params;
 
 typedef struct {
@@ -84,6 +86,19 @@ double or_log_prob(const float *x, const float *syn1, int32_t dim, const or_tree
 double or_log_prob_f64(const double *x, const double *syn1, int32_t dim, const or_tree *t, int32_t v);
 int or_loglik(const float *syn0, const float *syn1, const or_tree *t, const int32_t *tokens, int64_t n,
               const or_params *p, double *sum_ll, int64_t *n_pairs, int64_t *n_nodes);
+
+/* ---- negative sampling (the alternative objective named in §2; Ji et al.'s shared-negative
+        mini-batch, §3.2): syn1 is then the [V][dim] output vectors of the words ---- */
+int64_t or_noise_weights(const int64_t *vocab_counts, int32_t V, int64_t *weight);
+int or_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, int32_t *table);
+int64_t or_sample_negatives(const int32_t *tokens, int64_t n, const or_params *p, const int64_t *vocab_counts,
+                            const int32_t *table, int32_t log2_size, int32_t *negatives, int64_t cap,
+                            int64_t *n_kept, uint64_t *checksum);
+int or_train_ns(float *syn0, float *syn1, const int64_t *vocab_counts, const int32_t *table, int32_t log2_size,
+                const int32_t *tokens, int64_t n, const or_params *p, int64_t *stats);
+int or_ns_objective(const float *syn0, const float *syn1, const int64_t *vocab_counts, const int32_t *table,
+                    int32_t log2_size, const int32_t *tokens, int64_t n, const or_params *p, double *sum,
+                    int64_t *n_pairs, int64_t *n_terms);
 
 #ifdef __cplusplus
 }

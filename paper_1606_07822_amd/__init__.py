@@ -6,7 +6,8 @@ allocates device memory; workspaces are torch uint8 tensors made here.
 
 Entry points mirror the C ABI in include/w2v.h:
     build_vocab, build_huffman, train_hs_epoch, hs_loglik
-plus the test hooks sample_pairs and keep_thresholds.
+    build_noise_table, train_ns_epoch, ns_objective (negative sampling)
+plus the test hooks sample_pairs, keep_thresholds and sample_negatives.
 """
 from __future__ import annotations
 
@@ -44,7 +45,7 @@ class CParams(ctypes.Structure):
                 ("alpha0", ctypes.c_float), ("epoch", I32), ("n_epochs", I32), ("reserved1", I32),
                 ("corpus_tokens", I64), ("first_raw_index", I64), ("seed", U64), ("cache_k", I32),
                 ("flush_every", I32), ("sync_batch", I32), ("workers", I32), ("write_policy", I32),
-                ("flush_policy", I32), ("hot_k", I32), ("reserved2", I32 * 5)]
+                ("flush_policy", I32), ("hot_k", I32), ("negative", I32), ("reserved2", I32 * 4)]
 
 
 assert ctypes.sizeof(CModel) == 80 and ctypes.sizeof(CParams) == 112
@@ -91,6 +92,25 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_size_t, P]
         L.w2v_keep_thresholds.restype = ctypes.c_int
         L.w2v_keep_thresholds.argtypes = [P, I32, ctypes.c_double, I64, P, P]
+        L.w2v_noise_table_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_noise_table_workspace_bytes.argtypes = [I32]
+        L.w2v_build_noise_table.restype = ctypes.c_int
+        L.w2v_build_noise_table.argtypes = [P, I32, I32, P, P, P, ctypes.c_size_t, P]
+        L.w2v_train_ns_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_train_ns_workspace_bytes.argtypes = [ctypes.POINTER(CModel), I64, ctypes.POINTER(CParams)]
+        L.w2v_train_ns_epoch.restype = ctypes.c_int
+        L.w2v_train_ns_epoch.argtypes = [ctypes.POINTER(CModel), P, I32, P, I64, ctypes.POINTER(CParams), P, P,
+                                         ctypes.c_size_t, P]
+        L.w2v_ns_objective_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_ns_objective_workspace_bytes.argtypes = [ctypes.POINTER(CModel), I64, ctypes.POINTER(CParams)]
+        L.w2v_ns_objective.restype = ctypes.c_int
+        L.w2v_ns_objective.argtypes = [ctypes.POINTER(CModel), P, I32, P, I64, ctypes.POINTER(CParams), P, P, P, P,
+                                       ctypes.c_size_t, P]
+        L.w2v_sample_negatives_workspace_bytes.restype = ctypes.c_size_t
+        L.w2v_sample_negatives_workspace_bytes.argtypes = [I32, I64, ctypes.POINTER(CParams)]
+        L.w2v_sample_negatives.restype = ctypes.c_int
+        L.w2v_sample_negatives.argtypes = [P, I64, I32, P, I64, ctypes.POINTER(CParams), P, I32, P, I64, P, P, P,
+                                           ctypes.c_size_t, P]
         L.w2v_probe_rows.restype = ctypes.c_int
         L.w2v_probe_rows.argtypes = [P, I64, I32, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_float), P]
         _LIB = L
@@ -212,10 +232,11 @@ class Model:
     def c(self) -> CModel:
         for name, t in (("syn0", self.syn0), ("syn1", self.syn1)):
             _dev_ptr(t, torch.float32, name)
+        tr = self.tree
         return CModel(self.syn0.data_ptr(), self.syn1.data_ptr(), self.V, self.dim, self.stride, 0,
                       _dev_ptr(self.vocab_counts, torch.int64, "vocab_counts"), self.train_words,
-                      self.tree.codelen.data_ptr(), self.tree.code.data_ptr(), self.tree.point_off.data_ptr(),
-                      self.tree.points.data_ptr())
+                      tr.codelen.data_ptr() if tr else None, tr.code.data_ptr() if tr else None,
+                      tr.point_off.data_ptr() if tr else None, tr.points.data_ptr() if tr else None)
 
     def vectors(self) -> tuple[torch.Tensor, torch.Tensor]:
         """(syn0[:, :dim], syn1[:, :dim]) views."""
@@ -263,13 +284,14 @@ class Params:
     write_policy: int = 5
     flush_policy: int = 1
     hot_k: int | None = None
+    negative: int = 5
     extra: dict = field(default_factory=dict)
 
     def c(self) -> CParams:
         return CParams(self.arch, self.mode, self.window, self.doc_len, float(self.sample), float(self.alpha0),
                        self.epoch, self.n_epochs, 0, self.corpus_tokens, self.first_raw_index, self.seed,
                        self.cache_k, self.flush_every, self.sync_batch, self.workers, self.write_policy,
-                       self.flush_policy, self.resolved_hot_k())
+                       self.flush_policy, self.resolved_hot_k(), self.negative)
 
     def resolved_hot_k(self) -> int:
         if self.hot_k is not None:
@@ -390,3 +412,100 @@ def probe_rows(matrix: torch.Tensor, cols: int, mode: int, workgroups: int = 256
     _check(lib().w2v_probe_rows(_dev_ptr(matrix, torch.float32, "matrix"), matrix.shape[0], cols, matrix.shape[1],
                                 mode, workgroups, iters, ctypes.byref(ms), _stream(matrix.device)))
     return ms.value
+
+
+# ---------------------------------------------------------- negative sampling
+@dataclass
+class Noise:
+    table: torch.Tensor   # int32[2^log2_size] vocabulary indices
+    log2_size: int
+    total_weight: int
+
+
+def noise_log2_size(V: int) -> int:
+    """A table of about 64 entries per word: 2^ceil(log2(64 V)), between 2^10 and 2^27."""
+    return max(10, min(27, (64 * max(V, 1) - 1).bit_length()))
+
+
+def build_noise_table(vocab_counts: torch.Tensor, log2_size: int | None = None) -> Noise:
+    V = vocab_counts.numel()
+    L = noise_log2_size(V) if log2_size is None else log2_size
+    dev = vocab_counts.device
+    table = torch.empty(1 << L, dtype=torch.int32, device=dev)
+    ws = _workspace(lib().w2v_noise_table_workspace_bytes(V), dev)
+    tot = ctypes.c_int64(0)
+    _check(lib().w2v_build_noise_table(_dev_ptr(vocab_counts, torch.int64, "vocab_counts"), V, L, table.data_ptr(),
+                                       ctypes.byref(tot), ws.data_ptr(), ws.numel(), _stream(dev)))
+    return Noise(table, L, tot.value)
+
+
+def make_ns_model(syn0_init, syn1_init, vocab: Vocab, device="cuda") -> Model:
+    """[V, dim] input and output vectors in padded device rows (no tree)."""
+    s0 = torch.as_tensor(syn0_init, dtype=torch.float32)
+    s1 = torch.as_tensor(syn1_init, dtype=torch.float32)
+    V, dim = s0.shape
+    if tuple(s1.shape) != (V, dim):
+        raise ValueError("output vectors must be [V, dim]")
+    stride = padded_stride(dim)
+    syn0 = torch.zeros(V, stride, dtype=torch.float32, device=device)
+    syn1 = torch.zeros(V, stride, dtype=torch.float32, device=device)
+    syn0[:, :dim].copy_(s0)
+    syn1[:, :dim].copy_(s1)
+    return Model(syn0, syn1, dim, vocab.vocab_counts.contiguous(), vocab.train_words, None)
+
+
+def train_ns_epoch(model: Model, noise: Noise, tokens: torch.Tensor, p: Params,
+                   stats: torch.Tensor | None = None) -> torch.Tensor:
+    """One pass of skip-gram with shared negatives. Returns the device stats int64[5]; does not sync."""
+    dev = tokens.device
+    cm, cp = model.c(), p.c()
+    if cp.corpus_tokens <= 0:
+        cp.corpus_tokens = tokens.numel()
+    ws = _workspace(lib().w2v_train_ns_workspace_bytes(ctypes.byref(cm), tokens.numel(), ctypes.byref(cp)), dev)
+    if stats is None:
+        stats = torch.zeros(N_STATS, dtype=torch.int64, device=dev)
+    _check(lib().w2v_train_ns_epoch(ctypes.byref(cm), _dev_ptr(noise.table, torch.int32, "noise table"),
+                                    noise.log2_size, _dev_ptr(tokens, torch.int32, "tokens"), tokens.numel(),
+                                    ctypes.byref(cp), _dev_ptr(stats, torch.int64, "stats"), ws.data_ptr(),
+                                    ws.numel(), _stream(dev)))
+    return stats
+
+
+def ns_objective(model: Model, noise: Noise, tokens: torch.Tensor, p: Params):
+    """(sum of the negative-sampling objective over the sampler's pairs, n_pairs, n_terms). Synchronises."""
+    dev = tokens.device
+    cm, cp = model.c(), p.c()
+    ws = _workspace(lib().w2v_ns_objective_workspace_bytes(ctypes.byref(cm), tokens.numel(), ctypes.byref(cp)), dev)
+    s = ctypes.c_double(0)
+    npairs = ctypes.c_int64(0)
+    nt = ctypes.c_int64(0)
+    _check(lib().w2v_ns_objective(ctypes.byref(cm), _dev_ptr(noise.table, torch.int32, "noise table"),
+                                  noise.log2_size, _dev_ptr(tokens, torch.int32, "tokens"), tokens.numel(),
+                                  ctypes.byref(cp), ctypes.byref(s), ctypes.byref(npairs), ctypes.byref(nt),
+                                  ws.data_ptr(), ws.numel(), _stream(dev)))
+    return s.value, npairs.value, nt.value
+
+
+@dataclass
+class Negatives:
+    negatives: torch.Tensor | None   # int32[min(cap, kept), K], -1 = dropped
+    n_kept: int
+    checksum: int
+
+
+def sample_negatives(tokens: torch.Tensor, V: int, vocab_counts: torch.Tensor, train_words: int, p: Params,
+                     noise: Noise, cap: int = 0) -> Negatives:
+    dev = tokens.device
+    cp = p.c()
+    n = tokens.numel()
+    ws = _workspace(lib().w2v_sample_negatives_workspace_bytes(V, n, ctypes.byref(cp)), dev)
+    out = torch.empty(max(cap, 1) * p.negative, dtype=torch.int32, device=dev)
+    nk = ctypes.c_int64(0)
+    cs = ctypes.c_uint64(0)
+    _check(lib().w2v_sample_negatives(_dev_ptr(tokens, torch.int32, "tokens"), n, V,
+                                      _dev_ptr(vocab_counts, torch.int64, "vocab_counts"), train_words,
+                                      ctypes.byref(cp), _dev_ptr(noise.table, torch.int32, "noise table"),
+                                      noise.log2_size, out.data_ptr() if cap else None, cap, ctypes.byref(nk),
+                                      ctypes.byref(cs), ws.data_ptr(), ws.numel(), _stream(dev)))
+    m = min(cap, nk.value)
+    return Negatives(out[:m * p.negative].view(m, p.negative) if cap else None, nk.value, cs.value)

@@ -29,6 +29,21 @@ int run_train_sync(const w2v_model *m, const w2v_params *p, const SampleBufs &b,
                    const float *alpha_tab, int64_t blk0, unsigned long long *tstats, hipStream_t s);
 int run_probe_rows(float *matrix, int64_t rows, int32_t cols, int32_t row_stride, int32_t mode, int32_t workgroups,
                    int32_t iters, float *ms_host, hipStream_t s);
+size_t noise_workspace_bytes(int32_t V);
+int run_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, int32_t *table, int64_t *total_host,
+                    void *workspace, hipStream_t s);
+size_t ns_train_extra_bytes();
+int launch_train_ns(const w2v_model *m, const int32_t *table, int32_t log2_size, const w2v_params *p,
+                    const SampleBufs &b, int64_t n_tokens, const float *alpha_tab, int64_t blk0, Carve &c,
+                    hipEvent_t ev0, hipEvent_t ev1, int64_t *stats, hipStream_t s);
+size_t ns_objective_extra_bytes(int64_t n_docs);
+int run_ns_objective(const w2v_model *m, const int32_t *table, int32_t log2_size, const w2v_params *p,
+                     const SampleBufs &b, int64_t n_tokens, Carve &c, double *sum_host, int64_t *n_pairs_host,
+                     int64_t *n_terms_host, hipStream_t s);
+size_t ns_negatives_extra_bytes(int64_t n_docs);
+int run_ns_negatives(const w2v_params *p, const int32_t *table, int32_t log2_size, const SampleBufs &b,
+                     int64_t n_tokens, Carve &c, int32_t *out, int64_t cap, int64_t *n_kept_host,
+                     uint64_t *checksum_host, hipStream_t s);
 size_t loglik_extra_bytes(int64_t n_docs);
 int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
                double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, hipStream_t s);
@@ -140,6 +155,17 @@ int check_model(const w2v_model *m, bool need_tree) {
     if (m->train_words < 1) return fail(W2V_E_ARG, "train_words must be >= 1");
     if (need_tree && (!m->codelen || !m->code || !m->point_off || !m->points))
         return fail(W2V_E_ARG, "Huffman arrays are NULL");
+    return W2V_OK;
+}
+
+// negative sampling: the noise table and the number of negatives (dim bounds the register tiles)
+int check_ns(const w2v_model *m, const int32_t *table, int32_t log2_size, const w2v_params *p) {
+    if (!table) return fail(W2V_E_ARG, "noise_table is NULL");
+    if (log2_size < 1 || log2_size > 30) return fail(W2V_E_ARG, "log2_size must be in 1..30");
+    if (m && m->dim > 512) return fail(W2V_E_ARG, "negative sampling needs dim <= 512");
+    const int kmax = (m && m->dim > 320) ? 7 : 11;
+    if (p->negative < 1 || p->negative > kmax)
+        return fail(W2V_E_ARG, "negative must be in 1.." + std::to_string(kmax));
     return W2V_OK;
 }
 
@@ -346,6 +372,103 @@ int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, c
     SampleBufs b = sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
     if (int rc = launch_sampling(tokens, n_tokens, m->V, m->vocab_counts, m->train_words, p, b, nullptr, s)) return rc;
     return run_loglik(m, p, b, n_tokens, c, sum_ll_host, n_pairs_host, n_nodes_host, s);
+}
+
+size_t w2v_noise_table_workspace_bytes(int32_t V) { return V < 1 ? 0 : noise_workspace_bytes(V); }
+
+int w2v_build_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, int32_t *table,
+                          int64_t *total_weight_host, void *workspace, size_t workspace_bytes, void *hip_stream) {
+    g_err.clear();
+    if (V < 1 || V > (1 << 30)) return fail(W2V_E_ARG, "V must be in 1..2^30");
+    if (log2_size < 1 || log2_size > 30) return fail(W2V_E_ARG, "log2_size must be in 1..30");
+    if (!vocab_counts || !table || !total_weight_host) return fail(W2V_E_ARG, "a required pointer is NULL");
+    if (int rc = check_ws(workspace, workspace_bytes, noise_workspace_bytes(V))) return rc;
+    return run_noise_table(vocab_counts, V, log2_size, table, total_weight_host, workspace, as_stream(hip_stream));
+}
+
+size_t w2v_train_ns_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
+    if (!m || !p || p->doc_len < 1 || m->V < 2) return 0;
+    Carve c;
+    sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
+    c.take<float>(static_cast<size_t>(std::max<int64_t>(1, n_tokens) / 10000 + 3));   // alpha blocks
+    return c.used() + ns_train_extra_bytes();
+}
+
+int w2v_train_ns_epoch(const w2v_model *m, const int32_t *noise_table, int32_t log2_size, const int32_t *tokens,
+                       int64_t n_tokens, const w2v_params *p, int64_t *stats, void *workspace, size_t workspace_bytes,
+                       void *hip_stream) {
+    g_err.clear();
+    if (int rc = check_model(m, false)) return rc;
+    if (int rc = check_params(p, true)) return rc;
+    if (p->arch != 0 || p->mode != 0) return fail(W2V_E_ARG, "negative sampling trains skip-gram, mode 0, only");
+    if (int rc = check_ns(m, noise_table, log2_size, p)) return rc;
+    if (n_tokens < 0 || (n_tokens > 0 && !tokens)) return fail(W2V_E_ARG, "bad tokens / n_tokens");
+    if (int rc = check_ws(workspace, workspace_bytes, w2v_train_ns_workspace_bytes(m, n_tokens, p))) return rc;
+    hipStream_t s = as_stream(hip_stream);
+    Carve c(workspace);
+    SampleBufs b = sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
+    const int64_t span = std::max<int64_t>(1, n_tokens);
+    float *alpha_tab = c.take<float>(static_cast<size_t>(span / 10000 + 3));
+    if (int rc = launch_sampling(tokens, n_tokens, m->V, m->vocab_counts, m->train_words, p, b, nullptr, s)) return rc;
+    const int64_t eb = static_cast<int64_t>(p->epoch) * p->corpus_tokens;
+    const int64_t blk0 = (eb + p->first_raw_index) / 10000;
+    const int64_t blk1 = (eb + p->first_raw_index + span - 1) / 10000;
+    if (int rc = launch_alpha_table(p, blk0, blk1 - blk0 + 1, alpha_tab, s)) return rc;
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    if (int rc = timing_events(&ev0, &ev1)) return rc;
+    return launch_train_ns(m, noise_table, log2_size, p, b, n_tokens, alpha_tab, blk0, c, ev0, ev1, stats, s);
+}
+
+size_t w2v_ns_objective_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
+    if (!m || !p || p->doc_len < 1 || m->V < 2) return 0;
+    Carve c;
+    sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
+    return c.used() + ns_objective_extra_bytes(std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len)));
+}
+
+int w2v_ns_objective(const w2v_model *m, const int32_t *noise_table, int32_t log2_size, const int32_t *tokens,
+                     int64_t n_tokens, const w2v_params *p, double *sum_host, int64_t *n_pairs_host,
+                     int64_t *n_terms_host, void *workspace, size_t workspace_bytes, void *hip_stream) {
+    g_err.clear();
+    if (int rc = check_model(m, false)) return rc;
+    if (int rc = check_params(p, false)) return rc;
+    if (int rc = check_ns(m, noise_table, log2_size, p)) return rc;
+    if (n_tokens < 0 || (n_tokens > 0 && !tokens)) return fail(W2V_E_ARG, "bad tokens / n_tokens");
+    if (!sum_host || !n_pairs_host) return fail(W2V_E_ARG, "a required pointer is NULL");
+    if (int rc = check_ws(workspace, workspace_bytes, w2v_ns_objective_workspace_bytes(m, n_tokens, p))) return rc;
+    hipStream_t s = as_stream(hip_stream);
+    Carve c(workspace);
+    SampleBufs b = sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
+    if (int rc = launch_sampling(tokens, n_tokens, m->V, m->vocab_counts, m->train_words, p, b, nullptr, s)) return rc;
+    return run_ns_objective(m, noise_table, log2_size, p, b, n_tokens, c, sum_host, n_pairs_host, n_terms_host, s);
+}
+
+size_t w2v_sample_negatives_workspace_bytes(int32_t V, int64_t n_tokens, const w2v_params *p) {
+    if (!p || p->doc_len < 1 || V < 1) return 0;
+    Carve c;
+    sample_bufs_carve(c, V, n_tokens, p->doc_len);
+    return c.used() + ns_negatives_extra_bytes(std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len)));
+}
+
+int w2v_sample_negatives(const int32_t *tokens, int64_t n_tokens, int32_t V, const int64_t *vocab_counts,
+                         int64_t train_words, const w2v_params *p, const int32_t *noise_table, int32_t log2_size,
+                         int32_t *negatives, int64_t negatives_cap, int64_t *n_kept_host, uint64_t *checksum_host,
+                         void *workspace, size_t workspace_bytes, void *hip_stream) {
+    g_err.clear();
+    if (int rc = check_params(p, false)) return rc;
+    if (int rc = check_ns(nullptr, noise_table, log2_size, p)) return rc;
+    if (V < 1) return fail(W2V_E_ARG, "V must be >= 1");
+    if (n_tokens < 0 || (n_tokens > 0 && !tokens) || !vocab_counts) return fail(W2V_E_ARG, "bad tokens / counts");
+    if (!n_kept_host || !checksum_host) return fail(W2V_E_ARG, "a required pointer is NULL");
+    if (negatives_cap < 0) return fail(W2V_E_ARG, "negatives_cap must be >= 0");
+    if (p->sample > 0.0 && train_words < 1) return fail(W2V_E_ARG, "train_words must be >= 1 when sample > 0");
+    if (int rc = check_ws(workspace, workspace_bytes, w2v_sample_negatives_workspace_bytes(V, n_tokens, p))) return rc;
+    hipStream_t s = as_stream(hip_stream);
+    Carve c(workspace);
+    SampleBufs b = sample_bufs_carve(c, V, n_tokens, p->doc_len);
+    if (int rc = launch_sampling(tokens, n_tokens, V, vocab_counts, train_words, p, b, nullptr, s)) return rc;
+    return run_ns_negatives(p, noise_table, log2_size, b, n_tokens, c, negatives, negatives_cap, n_kept_host,
+                            checksum_host, s);
 }
 
 size_t w2v_sample_pairs_workspace_bytes(int32_t V, int64_t n_tokens, const w2v_params *p) {

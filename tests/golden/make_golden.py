@@ -19,6 +19,11 @@ learning rate decays over those N), and the result is stored as
 oracle_ll_<name>_first<N>.json: a bounded sample of a workload whose full
 epoch is too long for one core.
 
+With --ns K it trains skip-gram with K shared negatives instead (noise table
+of 2^ceil(log2(64 V)) entries, at least 2^10 and at most 2^27, output vectors
+starting at zero) and stores the held-out negative-sampling objective as
+oracle_ns<K>_<name>.json.
+
 With --sampler it stores, as oracle_sampler_<name>.json, digests of the
 oracle's vocabulary and Huffman tree for the whole corpus and the count and
 checksum of the training seed's (centre, context) pairs: the integer parts of
@@ -95,6 +100,51 @@ def run(name: str, cache_k: int = 31, flush_every: int = 10, train_tokens: int =
     }
 
 
+def noise_log2(V: int) -> int:
+    return max(10, min(27, (64 * V - 1).bit_length()))
+
+
+def run_ns(name: str, K: int) -> dict:
+    w = synth.WORKLOADS[name]
+    t0 = time.time()
+    tok = synth.workload_corpus(w)
+    held = synth.workload_corpus(w, heldout=True)
+    voc = oracle.build_vocab(tok, w.vocab, w.min_count)
+    tv = oracle.remap(tok, voc.id_to_vocab)
+    del tok
+    hv = oracle.remap(held, voc.id_to_vocab)
+    L = noise_log2(voc.V)
+    table = oracle.noise_table(voc.vocab_counts, L)
+    syn0, _ = synth.init_weights(voc.V, w.dim)
+    syn1 = np.zeros((voc.V, w.dim), np.float32)
+    pe = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, train_words=voc.train_words,
+                       seed=synth.SEED_EVAL, negative=K)
+    s0, npairs, nterms = oracle.ns_objective(syn0, syn1, voc.vocab_counts, table, L, hv, pe)
+    p = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, alpha0=w.alpha0, train_words=voc.train_words,
+                      corpus_tokens=tv.size, seed=synth.SEED_TRAIN, negative=K)
+    t1 = time.time()
+    st = oracle.train_ns(syn0, syn1, voc.vocab_counts, table, L, tv, p)
+    t2 = time.time()
+    s1, np1, nt1 = oracle.ns_objective(syn0, syn1, voc.vocab_counts, table, L, hv, pe)
+    assert (np1, nt1) == (npairs, nterms)
+    return {
+        "workload": name,
+        "negative": K,
+        "log2_table": L,
+        "V": voc.V,
+        "train_words": voc.train_words,
+        "dim": w.dim,
+        "stats": [int(x) for x in st],
+        "heldout_pairs": int(npairs),
+        "heldout_terms": int(nterms),
+        "init_mean_objective": s0 / npairs,
+        "mean_objective": s1 / npairs,
+        "oracle_source_sha256": hashlib.sha256(open(oracle.SRC_PATH, "rb").read()).hexdigest(),
+        "train_seconds_single_core": round(t2 - t1, 1),
+        "total_seconds": round(time.time() - t0, 1),
+    }
+
+
 def sampler(name: str) -> dict:
     w = synth.WORKLOADS[name]
     t0 = time.time()
@@ -151,8 +201,15 @@ if __name__ == "__main__":
     ap.add_argument("--sampler", action="store_true")
     ap.add_argument("--orient", type=int, default=0, help="1: the window word's path, the centre's vector as input")
     ap.add_argument("--epochs", type=int, default=1)
+    ap.add_argument("--ns", type=int, default=0, help="negatives per centre: train with negative sampling")
     a = ap.parse_args()
     for name in a.names:
+        if a.ns:
+            r = run_ns(name, a.ns)
+            with open(os.path.join(HERE, f"oracle_ns{a.ns}_{name}.json"), "w") as f:
+                json.dump(r, f, indent=1)
+            print(json.dumps(r), flush=True)
+            continue
         if a.sampler:
             r = sampler(name)
             with open(os.path.join(HERE, f"oracle_sampler_{name}.json"), "w") as f:

@@ -161,3 +161,65 @@ def test_probe_argument_errors(w2v, args, msg):
                                   ctypes.byref(ms), None)
     assert rc == w2v.W2V_E_ARG
     assert msg in w2v.last_error()
+
+
+def test_struct_offset_of_negative(w2v):
+    assert w2v.CParams.negative.offset == 92
+
+
+@pytest.mark.parametrize("mk,pk,table,L,msg", [
+    ({}, {}, 0, 20, "noise_table"),
+    ({}, {}, 0x9000, 0, "log2_size"),
+    ({}, {}, 0x9000, 31, "log2_size"),
+    ({}, dict(negative=0), 0x9000, 20, "negative"),
+    ({}, dict(negative=12), 0x9000, 20, "negative"),
+    (dict(dim=400, row_stride=448), dict(negative=8), 0x9000, 20, "negative"),
+    (dict(dim=600, row_stride=640), dict(negative=2), 0x9000, 20, "dim"),
+    ({}, dict(arch=1), 0x9000, 20, "skip-gram"),
+    ({}, dict(mode=1), 0x9000, 20, "skip-gram"),
+    ({}, dict(window=11), 0x9000, 20, "window"),
+])
+def test_train_ns_argument_errors(w2v, mk, pk, table, L, msg):
+    lib = w2v.lib()
+    m = _model(w2v, **mk)
+    p = _params(w2v, **pk)
+    rc = lib.w2v_train_ns_epoch(ctypes.byref(m), ctypes.c_void_p(table) if table else None, L,
+                                ctypes.c_void_p(0x8000), 1000, ctypes.byref(p), None, ctypes.c_void_p(0xA000), 1 << 30,
+                                None)
+    assert rc == w2v.W2V_E_ARG, w2v.last_error()
+    assert msg in w2v.last_error()
+
+
+def test_train_ns_needs_no_tree_but_a_workspace(w2v):
+    lib = w2v.lib()
+    m = _model(w2v, codelen=0, code=0, point_off=0, points=0)
+    p = _params(w2v)
+    need = lib.w2v_train_ns_workspace_bytes(ctypes.byref(m), 1000, ctypes.byref(p))
+    assert need > 0
+    rc = lib.w2v_train_ns_epoch(ctypes.byref(m), ctypes.c_void_p(0x9000), 20, ctypes.c_void_p(0x8000), 1000,
+                                ctypes.byref(p), None, ctypes.c_void_p(0xA000), need - 1, None)
+    assert rc == w2v.W2V_E_WORKSPACE
+
+
+def test_noise_table_and_objective_argument_errors(w2v):
+    lib = w2v.lib()
+    fake = ctypes.c_void_p(0x1000)
+    tot = ctypes.c_int64(0)
+    assert lib.w2v_build_noise_table(fake, 0, 10, fake, ctypes.byref(tot), fake, 1 << 20, None) == w2v.W2V_E_ARG
+    assert lib.w2v_build_noise_table(fake, 10, 0, fake, ctypes.byref(tot), fake, 1 << 20, None) == w2v.W2V_E_ARG
+    assert lib.w2v_build_noise_table(None, 10, 10, fake, ctypes.byref(tot), fake, 1 << 20, None) == w2v.W2V_E_ARG
+    need = lib.w2v_noise_table_workspace_bytes(1000)
+    assert need >= 2 * 1001 * 8
+    assert lib.w2v_build_noise_table(fake, 1000, 10, fake, ctypes.byref(tot), fake, need - 1,
+                                     None) == w2v.W2V_E_WORKSPACE
+    m = _model(w2v)
+    p = _params(w2v, negative=0)
+    s = ctypes.c_double(0)
+    n = ctypes.c_int64(0)
+    assert lib.w2v_ns_objective(ctypes.byref(m), fake, 10, fake, 100, ctypes.byref(p), ctypes.byref(s),
+                                ctypes.byref(n), None, fake, 1 << 30, None) == w2v.W2V_E_ARG
+    assert "negative" in w2v.last_error()
+    p = _params(w2v)
+    assert lib.w2v_sample_negatives(fake, 100, 10, fake, 100, ctypes.byref(p), None, 10, None, 0, ctypes.byref(n),
+                                    ctypes.byref(ctypes.c_uint64(0)), fake, 1 << 30, None) == w2v.W2V_E_ARG
+    assert "noise_table" in w2v.last_error()
