@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--sweep-cache", action="store_true",
                     help="instead of the benchmark line: one JSON line per (cache_k, flush_every) of the "
                          "cache-size x write-back-interval grid (epoch kernel time and held-out log-likelihood)")
+    ap.add_argument("--ns", type=int, default=0,
+                    help="measure skip-gram with this many shared negatives (negative sampling) instead of the "
+                         "hierarchical softmax; same workload and JSON layout, its own byte model")
     ap.add_argument("--sweep-k", default="0,1,3,7,15,31,63")
     ap.add_argument("--sweep-f", default="1,10,100,1000")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -100,6 +103,9 @@ def main():
     held_np = synth.workload_corpus(w, heldout=True, threads=16)
     log(f"generated {w.n_tokens:,} + {w.heldout_tokens:,} tokens in {time.time() - t0:.1f}s")
     tok = torch.from_numpy(tok_np).to(dev)
+
+    if args.ns:
+        return ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev)
 
     # first pass builds the model's shapes (same vocabulary every step: deterministic)
     voc = w2v.build_vocab(tok, w.vocab, w.min_count)
@@ -227,6 +233,127 @@ def main():
         "launch": {"workgroups": n_groups, "wavefronts": n_waves},
     }
     print(json.dumps(line), flush=True)
+
+
+def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
+    """Negative sampling on the same workload: one step = vocabulary + noise table + one epoch of
+    shared-negative training + held-out objective. Byte model per kept centre with P > 0 window words
+    and T targets (the centre word and its kept negatives): 8 d (P + T) (each row read once, then
+    changed once by an atomic add) + 4 K (table entries) + 9 (centre metadata)."""
+    import numpy as np
+    K = args.ns
+    voc = w2v.build_vocab(tok, w.vocab, w.min_count)
+    noise = w2v.build_noise_table(voc.vocab_counts)
+    syn0, _ = synth.init_weights(voc.V, w.dim)
+    model = w2v.make_ns_model(syn0, np.zeros((voc.V, w.dim), np.float32), voc, dev)
+    del syn0
+    p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
+                   seed=synth.SEED_TRAIN, negative=K, workers=args.workers)
+    pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL, negative=K)
+    held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
+    stats = torch.zeros(w2v.N_STATS, dtype=torch.int64, device=dev)
+
+    # byte model: every kept centre's targets (negatives hook) and which centres have window words
+    pr = w2v.sample_pairs(voc.tokens, voc.V, voc.vocab_counts, voc.train_words, p, cap=0, want_mask=True)
+    neg = w2v.sample_negatives(voc.tokens, voc.V, voc.vocab_counts, voc.train_words, p, noise, cap=pr.n_kept)
+    n = pr.keep_mask.numel()
+    n_docs = (n + p.doc_len - 1) // p.doc_len
+    m = torch.zeros(n_docs * p.doc_len, dtype=torch.bool, device=dev)
+    m[:n] = pr.keep_mask.bool()
+    per_doc = m.view(n_docs, p.doc_len).sum(1)
+    active = torch.repeat_interleave(per_doc >= 2, per_doc)          # kept centres, stream order
+    targets = int((1 + (neg.negatives[active] >= 0).sum(1)).sum().item())
+    centres = int(active.sum().item())
+    byte_total = 8 * w.dim * (pr.total + targets) + 4 * K * centres + 9 * centres
+    del pr, neg, m, active
+    torch.cuda.empty_cache()
+
+    def step():
+        v = w2v.build_vocab(tok, w.vocab, w.min_count)
+        nz = w2v.build_noise_table(v.vocab_counts)
+        model.vocab_counts = v.vocab_counts
+        w2v.train_ns_epoch(model, nz, v.tokens, p, stats=stats)
+        kms = w2v.last_train_kernel_ms()
+        obj = None if args.no_loglik else w2v.ns_objective(model, nz, held, pe)
+        return kms, obj
+
+    for i in range(args.warmup):
+        step()
+        log(f"warmup {i} done")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    kms_all, objs = [], []
+    for i in range(args.steps):
+        kms, obj = step()
+        kms_all.append(kms)
+        objs.append(obj)
+        log(f"step {i} train kernel {kms:.1f} ms")
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    st = stats.cpu().numpy()
+    ms_per_step = dt * 1e3 / args.steps
+    words = int(st[1])
+    kernel_ms = sum(kms_all) / len(kms_all)
+    achieved = byte_total / (kernel_ms / 1e3) / 1e9
+    n_groups, n_waves = w2v.last_train_launch()
+    cpu = None if args.no_cpu_baseline else cpu_baseline_ns(w, tok_np, args, K)
+    line = {
+        "metric": f"trained words/sec, skip-gram with {K} shared negatives V=1M d=300 fp32; % of HBM roofline",
+        "value": words / (ms_per_step / 1e3),
+        "unit": "words/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Zipf + topic-mixture corpus standing in for the paper's text corpus)",
+        "config": {"workload": args.workload, "tokens": w.n_tokens, "V": voc.V, "dim": w.dim, "window": w.window,
+                   "sample": w.sample, "negative": K, "noise_table_entries": int(noise.table.numel()),
+                   "step": "vocab + noise table + epoch" + ("" if args.no_loglik else " + held-out objective")},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None},
+        "train_kernel_ms": kernel_ms,
+        "train_kernel_words_per_s": words / (kernel_ms / 1e3),
+        "stats": dict(zip(("raw_tokens", "in_vocab_tokens", "kept_centres", "pairs", "pair_target_updates"),
+                          map(int, st))),
+        "algorithmic_bytes_per_launch": byte_total,
+        "heldout_mean_objective": (objs[-1][0] / objs[-1][1]) if objs and objs[-1] else None,
+        "cpu_baseline": cpu,
+        "launch": {"workgroups": n_groups, "wavefronts": n_waves},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline_ns(w, tok_np, args, K):
+    """The oracle's shared-negative training on a prefix of the same corpus, timed on this host."""
+    import numpy as np
+    import oracle
+    import synth
+    voc = oracle.build_vocab(tok_np, w.vocab, w.min_count)
+    L = max(10, min(27, (64 * voc.V - 1).bit_length()))
+    table = oracle.noise_table(voc.vocab_counts, L)
+    p = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, alpha0=w.alpha0, train_words=voc.train_words,
+                      corpus_tokens=w.n_tokens, seed=synth.SEED_TRAIN, negative=K)
+    syn0, _ = synth.init_weights(voc.V, w.dim)
+    syn1 = np.zeros((voc.V, w.dim), np.float32)
+    oracle.train_ns(syn0, syn1, voc.vocab_counts, table, L, oracle.remap(tok_np[:2 * w.doc_len], voc.id_to_vocab), p)
+    n_cal = 20 * w.doc_len
+    tv = oracle.remap(tok_np[:n_cal], voc.id_to_vocab)
+    t0 = time.perf_counter()
+    oracle.train_ns(syn0, syn1, voc.vocab_counts, table, L, tv, p)
+    per_tok = (time.perf_counter() - t0) / n_cal
+    n = int(min(w.n_tokens, max(n_cal, args.cpu_seconds / max(per_tok, 1e-9))))
+    n = (n // w.doc_len) * w.doc_len or n_cal
+    tv = oracle.remap(tok_np[:n], voc.id_to_vocab)
+    t0 = time.perf_counter()
+    st = oracle.train_ns(syn0, syn1, voc.vocab_counts, table, L, tv, p)
+    dt = time.perf_counter() - t0
+    return {"value": float(st[1]) / dt, "unit": "words/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n:,} tokens ({n // w.doc_len} documents) of the same corpus, one epoch of "
+                      f"shared-negative training (K={K}), {dt:.1f}s on one host core"}
 
 
 def sweep_cache(args, torch, w2v, synth, w, voc, tree, model, held, pe, ws, stats):

@@ -37,18 +37,18 @@
  *
  * Negative sampling (named in §2 as the alternative to the hierarchical
  * softmax; the opening of §3.2 describes Ji et al.'s mini-batch form of it):
- *   N1  the noise distribution is the unigram distribution raised to 3/4 (the
+ *   NS1  the noise distribution is the unigram distribution raised to 3/4 (the
  *       choice of Mikolov et al., whom §2 cites), with the weight of a word of
  *       count c taken in integers as isqrt(c * isqrt(c)), so that every
  *       implementation draws the same words.
- *   N2  noise table of T = 2^L entries: entry i holds the word v whose weight
+ *   NS2  noise table of T = 2^L entries: entry i holds the word v whose weight
  *       prefix sums satisfy Q[v] <= floor(i Q / T) < Q[v+1]; a draw r (32 bits)
  *       picks entry r >> (32 - L).
- *   N3  a centre's K negatives are shared by all of its window words (Ji et
+ *   NS3  a centre's K negatives are shared by all of its window words (Ji et
  *       al., §3.2): negative 4h+i is drawn from word i of Philox4x32-10 with
  *       counter (raw index lo, hi, epoch, 1 + h); a negative equal to the centre
  *       word is dropped.
- *   N4  mini-batch update (§3.2, level-3 BLAS form; §4.3 notes that it does
+ *   NS4  mini-batch update (§3.2, level-3 BLAS form; §4.3 notes that it does
  *       not use updated vectors within a mini-batch): with X the window words' vectors and Y
  *       the output vectors of the centre (label 1) and its negatives (label 0),
  *       S = X Y^T, G = alpha (labels - sigmoid(S)); X gains G Y and Y gains
@@ -676,8 +676,8 @@ int or_loglik(const float *syn0, const float *syn1, const or_tree *t, const int3
 }
 
 /* ------------------------------------------------------------------------ */
-/* Negative sampling: noise table (N1, N2), shared negatives (N3), mini-batch */
-/* updates (N4), objective.                                                   */
+/* Negative sampling: noise table (NS1, NS2), shared negatives (NS3), mini-batch */
+/* updates (NS4), objective.                                                   */
 /* ------------------------------------------------------------------------ */
 
 /* floor(sqrt(x)) for x < 2^62, by bisection on integers. */
@@ -690,7 +690,7 @@ static uint64_t isqrt_u64(uint64_t x) {
     return lo;
 }
 
-/* weight[v] = isqrt(c * isqrt(c)), c = count of v (N1); returns the total. */
+/* weight[v] = isqrt(c * isqrt(c)), c = count of v (NS1); returns the total. */
 int64_t or_noise_weights(const int64_t *vocab_counts, int32_t V, int64_t *weight) {
     int64_t tot = 0;
     for (int32_t v = 0; v < V; v++) {
@@ -701,7 +701,7 @@ int64_t or_noise_weights(const int64_t *vocab_counts, int32_t V, int64_t *weight
     return tot;
 }
 
-/* table[i] = v with Q[v] <= floor(i * Q / 2^L) < Q[v+1] (N2). Returns -1 on bad input. */
+/* table[i] = v with Q[v] <= floor(i * Q / 2^L) < Q[v+1] (NS2). Returns -1 on bad input. */
 int or_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, int32_t *table) {
     if (V < 1 || log2_size < 1 || log2_size > 30) return -1;
     int64_t *wt = (int64_t *)malloc(sizeof(int64_t) * (size_t)V);
@@ -720,7 +720,7 @@ int or_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, in
     return 0;
 }
 
-/* The K shared negatives of the centre at global raw index raw (N3); -1 where dropped. */
+/* The K shared negatives of the centre at global raw index raw (NS3); -1 where dropped. */
 static void draw_negatives(uint64_t seed, int64_t raw, int32_t epoch, int32_t K, const int32_t *table,
                            int32_t log2_size, int32_t centre, int32_t *neg) {
     uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
@@ -773,8 +773,8 @@ int64_t or_sample_negatives(const int32_t *tokens, int64_t n, const or_params *p
 }
 
 /*
- * One epoch of skip-gram with shared negatives, one sequential worker (N3,
- * N4). Per kept centre v with window words w_1..w_m and targets
+ * One epoch of skip-gram with shared negatives, one sequential worker (NS3,
+ * NS4). Per kept centre v with window words w_1..w_m and targets
  * t_0 = v (label 1), t_1..t_K its negatives (label 0, dropped ones skipped):
  *   s_qk = vector[w_q] . out[t_k],  g_qk = alpha (label_k - sigmoid(s_qk))
  *   dx_q = sum_k g_qk out[t_k],     dy_k = sum_q g_qk vector[w_q]

@@ -58,7 +58,7 @@ typedef struct {
     int32_t arch;             /* 0 = skip-gram, 1 = CBOW */
     int32_t sync_batch;       /* synchronous mode: centres per batch */
     int64_t max_centres;      /* stop after this many kept centres (-1 = all) */
-    int32_t negative;         /* negative sampling: negatives shared by a centre's window (N3) */
+    int32_t negative;         /* negative sampling: negatives shared by a centre's window (NS3) */
     int32_t reserved;
 } or_params;
 
