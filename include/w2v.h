@@ -241,9 +241,12 @@ int w2v_build_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_s
  * seed); one equal to v is dropped. With S_qk = syn0[w_q] . syn1[t_k] and
  * g_qk = alpha (label_k - sigmoid(S_qk)), syn0[w_q] gains sum_k g_qk
  * syn1[t_k] and syn1[t_k] gains sum_q g_qk syn0[w_q], all from the values
- * before the centre. Rows are changed with atomic adds; centres run
- * concurrently (lock-free), so results vary with scheduling except with
- * workers = 1. stats int64[W2V_N_STATS]: raw tokens, in-vocabulary tokens,
+ * before the centre. Write-back (p->write_policy): bit 0 set, a target row is
+ * stored as its value before the centre plus its change (lock-free, as in
+ * Hogwild: concurrent changes can be overwritten); bit 1 set, a word row is
+ * re-read and stored with its change; otherwise, and for a word or negative
+ * repeated within the centre, the change is added atomically. Centres run
+ * concurrently, so results vary with scheduling except with workers = 1. stats int64[W2V_N_STATS]: raw tokens, in-vocabulary tokens,
  * kept centres, pairs, pair-target updates. Asynchronous (mode 0) skip-gram
  * only; dim <= 512. Errors as w2v_train_hs_epoch, and W2V_E_ARG for a NULL
  * table, log2_size outside 1..30 or negative out of range.

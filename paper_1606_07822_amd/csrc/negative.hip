@@ -20,9 +20,13 @@
 // reduced four at a time (row j of the reduction holds target 4c+j), the
 // gradients go to LDS and their outer product with x accumulates the targets'
 // change in registers. A second pass over the window forms each word's change
-// from the gradients in LDS and the unchanged targets; both changes are added
-// to the model with atomic adds (rows can repeat within a centre: a negative
-// drawn twice, a word twice in the window). No MFMA: at P <= 20 window words
+// from the gradients in LDS and the unchanged targets. Target rows are
+// written back as stores of their value before the centre plus the change
+// (lock-free; the frequent words are negatives of many centres at once and
+// atomic adds to them were the kernel's main cost); word rows take atomic
+// adds of their change (or a re-read and store); a negative drawn twice or a
+// word twice in the window adds its second change atomically, so one worker
+// reproduces the sequential result. No MFMA: at P <= 20 window words
 // and K + 1 <= 12 targets the products are far too small for matrix tiles,
 // and the work is bound by the row traffic.
 #include <hip/hip_runtime.h>
@@ -34,7 +38,7 @@
 namespace w2v {
 namespace {
 
-constexpr int kNsWaves = 8;      // wavefronts per workgroup
+constexpr int kNsWaves = 4;      // wavefronts per workgroup (one per SIMD: occupancy in steps of one wave)
 constexpr int kMaxWindow = 20;   // window words per centre (2 * window, window <= 10)
 
 // ------------------------------------------------------------ noise table
@@ -159,6 +163,13 @@ __device__ __forceinline__ void atomic_add_row(float *p, const float (&r)[NE], i
 }
 
 template <int NE>
+__device__ __forceinline__ void store_row(float *p, const float (&r)[NE], int lane, int dim) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i)
+        if (lane + i * kWave < dim) p[lane + i * kWave] = r[i];
+}
+
+template <int NE>
 __device__ __forceinline__ float dot_partial(const float (&x)[NE], const float (&y)[NE]) {
     float s = 0.0f;
 #pragma unroll
@@ -193,6 +204,7 @@ struct NsArgs {
     const int32_t *table;
     int32_t log2_size, negative;
     int32_t workers;
+    int32_t write_policy;    // bit 0: target rows stored, bit 1: word rows stored (else atomic adds)
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, pair-target updates
     // objective
@@ -203,6 +215,7 @@ struct NsArgs {
 // NT target slots (K + 1 <= NT), rows of NE elements per lane.
 template <int NE, int NT>
 __global__ __launch_bounds__(kNsWaves *kWave) void k_train_ns(NsArgs a) {
+    constexpr int XR = NE <= 5 ? 3 : 2;   // window rows reloaded together in pass 2
     __shared__ float s_g[kNsWaves][kMaxWindow * NT];
     const int lane = lane_id();
     const int wid = static_cast<int>(threadIdx.x / kWave);
@@ -273,24 +286,62 @@ __global__ __launch_bounds__(kNsWaves *kWave) void k_train_ns(NsArgs a) {
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            // pass 2: each window word's change from the gradients and the unchanged targets
-            for (int p = 0; p < P; ++p) {
-                const int w = __builtin_amdgcn_readlane(wv, p);
-                float dx[NE];
+            // pass 2: each window word's change from the gradients and the unchanged targets. With
+            // write_policy bit 1 the first occurrence of a word stores its row plus the change (a reload,
+            // XR rows at a time), later occurrences in the same window add theirs atomically.
+            for (int p0 = 0; p0 < P; p0 += XR) {
+                float cur[XR][NE], dx[XR][NE];
+                bool st[XR];
 #pragma unroll
-                for (int i = 0; i < NE; ++i) dx[i] = 0.0f;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const float g = G[p * NT + t];
-#pragma unroll
-                    for (int i = 0; i < NE; ++i) dx[i] = fmaf(g, y[t][i], dx[i]);
+                for (int r = 0; r < XR; ++r) {
+                    const int p = p0 + r;
+                    st[r] = false;
+                    if (p < P) {
+                        const int w = __builtin_amdgcn_readlane(wv, p);
+                        const bool dup = __ballot(lane < p && wv == w) != 0ull;
+                        st[r] = (a.write_policy & 2) && !dup;
+                        if (st[r]) load_row<NE>(cur[r], a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
+                    }
                 }
-                atomic_add_row<NE>(a.syn0 + static_cast<int64_t>(w) * a.stride, dx, lane, a.dim);
+#pragma unroll
+                for (int r = 0; r < XR; ++r) {
+                    const int p = p0 + r;
+                    if (p < P) {
+#pragma unroll
+                        for (int i = 0; i < NE; ++i) dx[r][i] = 0.0f;
+#pragma unroll
+                        for (int t = 0; t < NT; ++t) {
+                            const float g = G[p * NT + t];
+#pragma unroll
+                            for (int i = 0; i < NE; ++i) dx[r][i] = fmaf(g, y[t][i], dx[r][i]);
+                        }
+                        float *row_p = a.syn0 + static_cast<int64_t>(__builtin_amdgcn_readlane(wv, p)) * a.stride;
+                        if (st[r]) {
+#pragma unroll
+                            for (int i = 0; i < NE; ++i) cur[r][i] += dx[r][i];
+                            store_row<NE>(row_p, cur[r], lane, a.dim);
+                        } else {
+                            atomic_add_row<NE>(row_p, dx[r], lane, a.dim);
+                        }
+                    }
+                }
             }
+            // targets: with write_policy bit 0 the first slot of a word stores the snapshot plus its change
+            // (no reload), a repeated negative adds its change atomically
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const int n = __builtin_amdgcn_readlane(tg, t);
-                if (n >= 0) atomic_add_row<NE>(a.syn1 + static_cast<int64_t>(n) * a.stride, dy[t], lane, a.dim);
+                if (n >= 0) {
+                    float *row_n = a.syn1 + static_cast<int64_t>(n) * a.stride;
+                    const bool dup = __ballot(lane < t && tg == n) != 0ull;
+                    if ((a.write_policy & 1) && !dup) {
+#pragma unroll
+                        for (int i = 0; i < NE; ++i) y[t][i] += dy[t][i];
+                        store_row<NE>(row_n, y[t], lane, a.dim);
+                    } else {
+                        atomic_add_row<NE>(row_n, dy[t], lane, a.dim);
+                    }
+                }
             }
             __builtin_amdgcn_wave_barrier();
             n_pairs += P;
@@ -501,6 +552,7 @@ NsArgs ns_args(const w2v_model *m, const int32_t *table, int32_t log2_size, cons
     a.table = table;
     a.log2_size = log2_size;
     a.negative = p->negative;
+    a.write_policy = p->write_policy;
     return a;
 }
 

@@ -45,17 +45,19 @@ def _bench_line(path: str) -> dict:
 def stats(args):
     rows = list(csv.DictReader(open(args.csv)))
     b = _bench_line(args.bench)
-    out = [f"# rocprofv3 kernel statistics: {b['config']['workload']} (default bench)", "",
+    title = args.title or f"{b['config']['workload']} (default bench)"
+    out = [f"# rocprofv3 kernel statistics: {title}", "",
            "Command (repository root, MI355X):", f"  {args.command}", "",
            f"bench.py: --steps {b['steps']} --warmup {b['warmup']}; one step = {b['config']['step']}.", "",
            f"{'kernel':<72}{'calls':>6}{'total ms':>12}{'avg ms':>12}{'%':>7}"]
     for r in rows:
         out.append(f"{_short(r['Name']):<72}{int(r['Calls']):>6}{float(r['TotalDurationNs']) / 1e6:>12.2f}"
                    f"{float(r['AverageNs']) / 1e6:>12.3f}{float(r['Percentage']):>7.2f}")
-    train = [r for r in rows if "k_train<" in r["Name"]]
+    train = [r for r in rows if "k_train" in r["Name"] and "<" in r["Name"]]
     out += ["", "bench.py line of the same run (HIP events on the training kernel's stream):",
             f"  train_kernel_ms = {b['train_kernel_ms']:.1f}"
-            + (f"  (rocprofv3 average of k_train above: {float(train[0]['AverageNs']) / 1e6:.1f})" if train else ""),
+            + (f"  (rocprofv3 average of the training kernel above: {float(train[0]['AverageNs']) / 1e6:.1f})"
+               if train else ""),
             f"  value = {b['value']:.4g} {b['unit']}, ms_per_step = {b['ms_per_step']:.1f}",
             f"  roofline = {json.dumps(b['roofline'])}"]
     if b.get("memory_probe"):
@@ -140,6 +142,7 @@ def main():
     s.add_argument("bench")
     s.add_argument("out")
     s.add_argument("--command", required=True)
+    s.add_argument("--title", default="")
     t = sub.add_parser("traffic")
     for a in ("fetch", "write", "bench", "out_json", "out_txt"):
         t.add_argument(a)

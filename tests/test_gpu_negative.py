@@ -84,10 +84,14 @@ def test_negatives_bit_exact(w2v, K, n, kw):
 
 # One wavefront reproduces the oracle up to rounding; dim picks the elements per lane (2, 5, 8), K the
 # number of target slots (4, 8, 12).
-@pytest.mark.parametrize("K,dim,win,docs", [(5, 100, 5, 5), (1, 100, 5, 3), (3, 300, 5, 3), (5, 300, 5, 3),
-                                            (11, 300, 10, 2), (7, 450, 5, 2), (2, 50, 2, 4)])
-def test_single_worker_matches_oracle(w2v, K, dim, win, docs):
-    log(f"ns single worker K={K} dim={dim} window={win}")
+# write_policy: 0 = atomic adds everywhere, 1 = target rows stored, 3 = word rows stored too (a repeated word or
+# negative adds its change atomically, so one worker still matches the oracle).
+@pytest.mark.parametrize("K,dim,win,docs,wp", [(5, 100, 5, 5, 0), (5, 100, 5, 5, 3), (1, 100, 5, 3, 1),
+                                               (3, 300, 5, 3, 3), (5, 300, 5, 3, 0), (5, 300, 5, 3, 3),
+                                               (11, 300, 10, 2, 3), (7, 450, 5, 2, 3), (7, 450, 5, 2, 0),
+                                               (2, 50, 2, 4, 1)])
+def test_single_worker_matches_oracle(w2v, K, dim, win, docs, wp):
+    log(f"ns single worker K={K} dim={dim} window={win} write_policy={wp}")
     s = oracle_side("sg_v30k_d100")
     tv = s.tv[:docs * 1000]
     voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
@@ -102,7 +106,7 @@ def test_single_worker_matches_oracle(w2v, K, dim, win, docs):
                        corpus_tokens=s.tv.size, negative=K)
     ost = oracle.train_ns(a0, a1, s.voc.vocab_counts, table, L, tv, op)
     model = w2v.make_ns_model(syn0, syn1, voc)
-    p = w2v.Params(window=win, sample=1e-3, corpus_tokens=s.tv.size, negative=K, workers=1)
+    p = w2v.Params(window=win, sample=1e-3, corpus_tokens=s.tv.size, negative=K, workers=1, write_policy=wp)
     st = w2v.train_ns_epoch(model, noise, to_dev(tv), p).cpu().numpy()
     assert list(st) == list(ost)
     g0, g1 = (t.cpu().numpy() for t in model.vectors())
@@ -143,7 +147,7 @@ def test_objective_at_zero_output_vectors_closed_form(w2v):
     assert abs(sg + math.log(2.0) * nterms) <= 1e-9 * nterms
 
 
-@pytest.mark.parametrize("kw", [{}, dict(workers=256)])
+@pytest.mark.parametrize("kw", [dict(write_policy=3), dict(write_policy=0), dict(write_policy=3, workers=256)])
 def test_async_objective_within_1pct_of_stored_oracle(w2v, kw):
     name = "sg_v30k_d100"
     path = os.path.join(GOLDEN, f"oracle_ns5_{name}.json")
