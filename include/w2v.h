@@ -137,7 +137,8 @@ typedef struct {
     int32_t workers;         /* wavefronts that take documents; 0 = fill the GPU; 1 = one sequential worker */
     int32_t write_policy;    /* bit 0: uncached inner-node rows are stored (lock-free, concurrent updates may be
                                 overwritten, as in Hogwild) instead of atomically adding their change;
-                                bit 1: the same for the word vectors syn0;
+                                bit 1: the same for the word vectors syn0 (a word repeated within a window
+                                stores at its first position and adds the change of the others);
                                 bit 2: the same for the cached rows in the workgroup's LDS copy */
     int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), 1 = add the
                                 change divided by the number of workgroups (their progress averaged) */

@@ -431,7 +431,10 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                                 if (p < nx) {
                                     const int w = __builtin_amdgcn_readlane(wv, g0 + p);
                                     float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
-                                    if (a.write_policy & 2) {
+                                    // a word repeated in the window: its first position stores the row
+                                    // read before the centre plus its change, later ones add theirs
+                                    const bool rep = (a.write_policy & 2) && __ballot(lane < g0 + p && wv == w) != 0ull;
+                                    if ((a.write_policy & 2) && !rep) {
                                         float nx_[NE];
 #pragma unroll
                                         for (int i = 0; i < NE; ++i) nx_[i] = x[p][i] + e[p][i];

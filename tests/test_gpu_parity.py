@@ -261,7 +261,8 @@ def test_sync_mode_is_deterministic(w2v):
 # One wavefront reproduces the oracle's centre-major order up to rounding. dim picks the kernel variant
 # (elements per lane 2, 4, 5, 8, 16; up to 256 columns every chunk is prefetched, above only past the
 # cached prefix); write_policy 0 (atomic adds of the change), 1 (row stores) and 5 (row stores, cached rows
-# included) take different write-back paths; window 10 gives skip-gram windows wider than one register group at dim >= 200 (parked gradients).
+# included) take different write-back paths, 7 and 2 store word vectors too (a word repeated in a window adds
+# atomically); window 10 gives skip-gram windows wider than one register group at dim >= 200 (parked gradients).
 @pytest.mark.parametrize("arch,k,F,ndocs,dim,wp,win", [
     (0, 0, 10, 5, 100, 1, 5), (0, 31, 10, 5, 100, 1, 5), (0, 7, 1, 5, 100, 1, 5), (1, 0, 10, 5, 100, 1, 5),
     (1, 31, 10, 5, 100, 1, 5),
@@ -272,6 +273,7 @@ def test_sync_mode_is_deterministic(w2v):
     (1, 31, 10, 2, 600, 1, 5), (0, 15, 10, 2, 1024, 0, 3),
     (0, 31, 10, 5, 100, 5, 5), (0, 31, 10, 3, 300, 5, 5), (0, 31, 10, 2, 300, 5, 10), (1, 31, 10, 3, 300, 5, 5),
     (0, 31, 10, 2, 450, 5, 5),
+    (0, 31, 10, 5, 100, 7, 5), (0, 31, 10, 5, 300, 7, 5), (0, 0, 10, 3, 300, 2, 5), (1, 31, 10, 3, 300, 7, 5),
 ])
 def test_single_worker_matches_oracle_centre_major(w2v, arch, k, F, ndocs, dim, wp, win):
     log(f"single worker arch={arch} k={k} F={F} docs={ndocs} dim={dim} write_policy={wp} window={win}")
