@@ -1,0 +1,156 @@
+"""Degenerate and boundary inputs of the training and evaluation paths on the
+GPU (through the C ABI): empty and fully dropped streams, documents too short
+for a window, the smallest tree (V = 2) and vector size (d = 1), a ragged last
+document, a corpus fed in whole-document chunks, and the widest window.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_common import oracle_side, row_rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def w2v():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1606_07822_amd as w2v
+    w2v.lib()
+    return w2v
+
+
+def to_dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def tiny_model(w2v, s, dim=16):
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.1)
+    return voc, tree, syn0, syn1
+
+
+@pytest.mark.parametrize("mode,arch", [(0, 0), (0, 1), (0, 2), (1, 0)])
+@pytest.mark.parametrize("case", ["empty", "all_dropped", "doc_len_1"])
+def test_nothing_to_train_leaves_the_model_alone(w2v, mode, arch, case):
+    s = oracle_side("tiny_sg_v1k_d50")
+    voc, tree, syn0, syn1 = tiny_model(w2v, s)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    before = [t.cpu().numpy().copy() for t in model.vectors()]
+    doc_len = 1000
+    if case == "empty":
+        tok = to_dev(np.zeros(1, np.int32))[:0]
+    elif case == "all_dropped":
+        tok = to_dev(np.full(2500, -1, np.int32))
+    else:
+        tok = to_dev(s.tv[:3000])
+        doc_len = 1                       # one token per document: centres without window words
+    p = w2v.Params(window=2, mode=mode, arch=arch, doc_len=doc_len, corpus_tokens=max(1, tok.numel()), cache_k=7)
+    st = w2v.train_hs_epoch(model, tok, p).cpu().numpy()
+    n = tok.numel()
+    assert st[0] == n and st[3] == 0 and st[4] == 0
+    assert st[1] == (0 if case != "doc_len_1" else int((s.tv[:3000] >= 0).sum()))
+    for a, b in zip(before, (t.cpu().numpy() for t in model.vectors())):
+        np.testing.assert_array_equal(a, b)
+    sg, npairs, nnodes = w2v.hs_loglik(model, tok, w2v.Params(window=2, doc_len=doc_len))
+    assert (sg, npairs, nnodes) == (0.0, 0, 0)
+
+
+def test_negative_sampling_on_empty_stream(w2v):
+    s = oracle_side("tiny_sg_v1k_d50")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    noise = w2v.build_noise_table(voc.vocab_counts)
+    syn0, _ = synth.init_weights(s.voc.V, 8)
+    model = w2v.make_ns_model(syn0, np.ones((s.voc.V, 8), np.float32), voc)
+    tok = to_dev(np.zeros(1, np.int32))[:0]
+    st = w2v.train_ns_epoch(model, noise, tok, w2v.Params(window=2, corpus_tokens=1)).cpu().numpy()
+    assert list(st) == [0, 0, 0, 0, 0]
+    np.testing.assert_array_equal(model.vectors()[0].cpu().numpy(), syn0)
+    assert w2v.ns_objective(model, noise, tok, w2v.Params(window=2)) == (0.0, 0, 0)
+
+
+@pytest.mark.parametrize("dim", [1, 3, 64])
+def test_two_word_vocabulary(w2v, dim):
+    # the smallest tree: one inner node, codes {0} and {1}
+    rng = np.random.default_rng(dim)
+    tok = rng.choice([3, 7], size=4000, p=[0.6, 0.4]).astype(np.int32)
+    voc = w2v.build_vocab(to_dev(tok), 10, 1)
+    assert voc.V == 2
+    tree = w2v.build_huffman(voc.vocab_counts)
+    ov = oracle.build_vocab(tok, 10, 1)
+    ot = oracle.build_huffman(ov.vocab_counts)
+    tv = oracle.remap(tok, ov.id_to_vocab)
+    syn0, syn1 = synth.init_weights(2, dim, syn1_scale=0.2)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(2, dim, window=3, train_words=ov.train_words, corpus_tokens=tok.size, order=1, cache_k=1,
+                       flush_every=10)
+    ost = oracle.train(a0, a1, ot, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=3, corpus_tokens=tok.size, workers=1, cache_k=1, flush_every=10)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:1], a1) <= 1e-4
+
+
+@pytest.mark.parametrize("n", [1, 999, 2500, 3001])
+def test_ragged_last_document(w2v, n):
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = s.tv[:n]
+    syn0, syn1 = synth.init_weights(s.voc.V, 100, syn1_scale=0.005)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, 100, window=5, sample=1e-3, train_words=s.voc.train_words, corpus_tokens=s.tv.size,
+                       order=1, cache_k=31, flush_every=10)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=31, flush_every=10)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+@pytest.mark.parametrize("arch", [0, 2])
+def test_chunked_stream_equals_whole_stream(w2v, arch):
+    # without a cache one worker's result depends only on the centre sequence and the raw positions,
+    # so feeding whole documents in two calls (first_raw_index) gives the same bits
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = to_dev(s.tv[:6000])
+    syn0, syn1 = synth.init_weights(s.voc.V, 64, syn1_scale=0.01)
+    m1 = w2v.make_model(syn0, syn1, voc, tree)
+    m2 = w2v.make_model(syn0, syn1, voc, tree)
+    base = dict(window=5, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=0, arch=arch)
+    st = w2v.train_hs_epoch(m1, tv, w2v.Params(**base)).cpu().numpy()
+    sa = w2v.train_hs_epoch(m2, tv[:4000], w2v.Params(**base)).cpu().numpy()
+    sb = w2v.train_hs_epoch(m2, tv[4000:], w2v.Params(first_raw_index=4000, **base)).cpu().numpy()
+    assert list(st) == list(sa + sb)
+    for a, b in zip(m1.vectors(), m2.vectors()):
+        np.testing.assert_array_equal(a.cpu().numpy(), b.cpu().numpy())
+
+
+def test_widest_window_and_widest_rows(w2v):
+    # window 10 (up to 20 window words, two register groups) at the widest vector size, d = 1024
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = s.tv[:2000]
+    syn0, syn1 = synth.init_weights(s.voc.V, 1024, syn1_scale=0.5 / 1024)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, 1024, window=10, sample=1e-3, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, order=1, cache_k=15, flush_every=10)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=10, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=15, flush_every=10)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
