@@ -20,7 +20,7 @@ size_t pairs_workspace_bytes(int32_t V, int64_t n_tokens, int32_t doc_len);
 int run_sample_pairs(const int32_t *, int64_t, int32_t, const int64_t *, int64_t, const w2v_params *, int64_t *,
                      int64_t *, int64_t, uint8_t *, int64_t *, int64_t *, uint64_t *, void *, hipStream_t);
 size_t train_lds_bytes(int32_t cache_k, int32_t dim);
-int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_docs, int *grid, int *waves);
+int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_units, int *grid, int *waves);
 int64_t train_egrad_floats(int arch, int dim, int stride, int window, int waves);
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals);
@@ -195,7 +195,8 @@ int64_t egrad_floats(const w2v_model *m, int64_t n_tokens, const w2v_params *p) 
     if (p->mode != 0) return 0;
     int grid = 0, waves = 0;
     const int64_t n_docs = n_tokens > 0 ? ceil_div(n_tokens, static_cast<int64_t>(p->doc_len)) : 0;
-    if (train_launch_shape(p->arch, m->dim, p->cache_k, p->workers, n_docs, &grid, &waves)) return 0;
+    if (train_launch_shape(p->arch, m->dim, p->cache_k, p->workers, n_docs * segs_per_doc(p->doc_len), &grid, &waves))
+        return 0;
     return train_egrad_floats(p->arch, m->dim, m->row_stride, p->window, waves);
 }
 
@@ -270,6 +271,8 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     if (lds + 1024 > device_max_lds())
         return fail(W2V_E_ARG, "cache does not fit LDS: 2 * cache_k rows = " + std::to_string(lds) + " bytes");
     if (int rc = check_ws(workspace, workspace_bytes, train_bytes(m, n_tokens, p))) return rc;
+    if (ceil_div(std::max<int64_t>(0, n_tokens), p->doc_len) * segs_per_doc(p->doc_len) > INT32_MAX)
+        return fail(W2V_E_ARG, "too many documents for one call: split the stream (first_raw_index)");
     hipStream_t s = as_stream(hip_stream);
     Carve c(workspace);
     SampleBufs b = sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
@@ -312,6 +315,9 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     a.doc_kept = b.doc_kept;
     a.n_docs = n_tokens > 0 ? ceil_div(n_tokens, p->doc_len) : 0;
     a.doc_len = p->doc_len;
+    a.seg_len = kSegLen;
+    a.segs_per_doc = segs_per_doc(p->doc_len);
+    a.n_units = a.n_docs * a.segs_per_doc;
     a.first_raw = p->first_raw_index;
     a.epoch_base = eb;
     a.alpha_tab = alpha_tab;
@@ -404,6 +410,8 @@ int w2v_train_ns_epoch(const w2v_model *m, const int32_t *noise_table, int32_t l
     if (int rc = check_ns(m, noise_table, log2_size, p)) return rc;
     if (n_tokens < 0 || (n_tokens > 0 && !tokens)) return fail(W2V_E_ARG, "bad tokens / n_tokens");
     if (int rc = check_ws(workspace, workspace_bytes, w2v_train_ns_workspace_bytes(m, n_tokens, p))) return rc;
+    if (ceil_div(std::max<int64_t>(0, n_tokens), p->doc_len) * segs_per_doc(p->doc_len) > INT32_MAX)
+        return fail(W2V_E_ARG, "too many documents for one call: split the stream (first_raw_index)");
     hipStream_t s = as_stream(hip_stream);
     Carve c(workspace);
     SampleBufs b = sample_bufs_carve(c, m->V, n_tokens, p->doc_len);

@@ -34,7 +34,7 @@ __device__ __forceinline__ int64_t leaf_val(const int64_t *__restrict__ counts, 
 __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__restrict__ counts, int32_t V,
                                                               int32_t *__restrict__ parent, uint8_t *__restrict__ bit,
                                                               int64_t *__restrict__ icount, int32_t *__restrict__ flags) {
-    __shared__ int32_t s_pl, s_ih, s_a, s_mode, s_m;
+    __shared__ int32_t s_pl, s_ih, s_a, s_mode;
     __shared__ int64_t s_front;
     const int tid = threadIdx.x;
     if (tid == 0) {

@@ -195,6 +195,8 @@ struct NsArgs {
     const int32_t *doc_kept;
     int64_t n_docs;
     int32_t doc_len;
+    int32_t segs_per_doc;    // work unit: kSegLen consecutive kept centres of one document
+    int64_t n_units;
     int64_t first_raw;
     int64_t epoch_base;
     int32_t epoch;
@@ -224,15 +226,19 @@ __global__ __launch_bounds__(kNsWaves *kWave) void k_train_ns(NsArgs a) {
     if (gw >= a.workers) return;
     uint64_t n_kept = 0, n_pairs = 0, n_upd = 0;
     while (true) {
-        int doc = 0;
-        if (lane == 0) doc = atomicAdd(a.queue, 1);
-        doc = __builtin_amdgcn_readfirstlane(doc);
-        if (doc >= a.n_docs) break;
+        int unit = 0;
+        if (lane == 0) unit = atomicAdd(a.queue, 1);
+        unit = __builtin_amdgcn_readfirstlane(unit);
+        if (unit >= a.n_units) break;
+        const int doc = unit / a.segs_per_doc;
         const int nk = a.doc_kept[doc];
+        const int j0 = (unit - doc * a.segs_per_doc) * kSegLen;
+        if (j0 >= nk) continue;
+        const int j1 = min(nk, j0 + kSegLen);
         const int64_t base = static_cast<int64_t>(doc) * a.doc_len;
         const int32_t *kv = a.kept_vid + base;
         const uint32_t *km = a.kept_meta + base;
-        for (int j = 0; j < nk; ++j) {
+        for (int j = j0; j < j1; ++j) {
             const uint32_t meta = km[j];
             const int v = kv[j];
             const int eff = static_cast<int>(meta >> 16);
@@ -545,6 +551,8 @@ NsArgs ns_args(const w2v_model *m, const int32_t *table, int32_t log2_size, cons
     a.doc_kept = b.doc_kept;
     a.n_docs = n_tokens > 0 ? ceil_div(n_tokens, p->doc_len) : 0;
     a.doc_len = p->doc_len;
+    a.segs_per_doc = segs_per_doc(p->doc_len);
+    a.n_units = a.n_docs * a.segs_per_doc;
     a.first_raw = p->first_raw_index;
     a.epoch_base = static_cast<int64_t>(p->epoch) * p->corpus_tokens;
     a.epoch = p->epoch;
@@ -610,7 +618,9 @@ int launch_train_ns(const w2v_model *m, const int32_t *table, int32_t log2_size,
                                                          kNsWaves * kWave, 0));
     int64_t grid = static_cast<int64_t>(device_cu_count()) * std::max(1, per_cu);
     if (p->workers > 0) grid = ceil_div(p->workers, kNsWaves);
-    grid = std::max<int64_t>(1, std::min<int64_t>(grid, std::max<int64_t>(1, ceil_div(a.n_docs, kNsWaves))));
+    // at least kMinUnits work units per wavefront
+    constexpr int kMinUnits = 8;
+    grid = std::max<int64_t>(1, std::min<int64_t>(grid, ceil_div(a.n_units, int64_t(kNsWaves) * kMinUnits)));
     a.workers = p->workers > 0 ? p->workers : static_cast<int32_t>(grid * kNsWaves);
     record_train_launch(static_cast<int>(grid), a.workers);
     k_zero_ns<<<1, 64, 0, s>>>(a.queue, a.stats);

@@ -38,7 +38,7 @@ namespace w2v {
 namespace {
 
 constexpr int kChunk = 4;            // inner nodes per step (one per 16-lane row)
-constexpr int kMinDocsPerWave = 8;   // automatic launch size: documents per wavefront, at least
+constexpr int kMinUnitsPerWave = 8;  // automatic launch size: work units (document segments) per wavefront, at least
 
 __device__ __forceinline__ float sigmoid_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
@@ -265,7 +265,8 @@ __device__ __forceinline__ void chunk_write_delta(const TrainArgs &a, float *val
 //               stored, need no copy, and those registers hold the prefetched
 //               next chunk instead. With every row stored the whole path is
 //               prefetched.
-constexpr int kPfNone = 0, kPfAll = 1, kPfSuffix = 2;
+[[maybe_unused]] constexpr int kPfNone = 0;
+constexpr int kPfAll = 1, kPfSuffix = 2;
 
 // Walk the path of the centre with the inputs x[0..nx) (in order), accumulating
 // the hidden-layer gradients into e[0..nx). PG = compile-time bound of nx.
@@ -370,15 +371,19 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     uint64_t n_kept = 0, n_pairs = 0, n_nodes = 0;
     if (gw < a.workers) {
         while (true) {
-            int doc = 0;
-            if (lane == 0) doc = atomicAdd(a.queue, 1);
-            doc = __builtin_amdgcn_readfirstlane(doc);
-            if (doc >= a.n_docs) break;
+            int unit = 0;
+            if (lane == 0) unit = atomicAdd(a.queue, 1);
+            unit = __builtin_amdgcn_readfirstlane(unit);
+            if (unit >= a.n_units) break;
+            const int doc = unit / a.segs_per_doc;
             const int nk = a.doc_kept[doc];
+            const int j0 = (unit - doc * a.segs_per_doc) * a.seg_len;
+            if (j0 >= nk) continue;
+            const int j1 = min(nk, j0 + a.seg_len);
             const int64_t base = static_cast<int64_t>(doc) * a.doc_len;
             const int32_t *kv = a.kept_vid + base;
             const uint32_t *km = a.kept_meta + base;
-            for (int j = 0; j < nk; ++j) {
+            for (int j = j0; j < j1; ++j) {
                 const uint32_t meta = km[j];
                 const int v = kv[j];
                 const int eff = static_cast<int>(meta >> 16);
@@ -605,7 +610,7 @@ size_t train_lds_bytes(int32_t cache_k, int32_t dim) {
     return 2ull * cache_k * v.ls(dim) * sizeof(float);
 }
 
-int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_docs, int *grid, int *waves) {
+int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_units, int *grid, int *waves) {
     const Variant v = pick_variant(arch, dim);
     if (workers > 0) {
         *grid = static_cast<int>(ceil_div(workers, v.waves_per_block));
@@ -617,10 +622,10 @@ int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_do
     W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(v.fn),
                                                          v.waves_per_block * kWave, lds));
     int64_t g = static_cast<int64_t>(device_cu_count()) * std::max(1, per_cu);
-    // every wavefront gets at least kMinDocsPerWave documents, so that every workgroup
+    // every wavefront gets at least kMinUnitsPerWave work units, so that every workgroup
     // (cache owner) contributes to the averaged write-back of the cached rows
-    const int64_t by_docs = ceil_div(n_docs, static_cast<int64_t>(v.waves_per_block) * kMinDocsPerWave);
-    g = std::max<int64_t>(1, std::min<int64_t>(g, by_docs));
+    const int64_t by_units = ceil_div(n_units, static_cast<int64_t>(v.waves_per_block) * kMinUnitsPerWave);
+    g = std::max<int64_t>(1, std::min<int64_t>(g, by_units));
     *grid = static_cast<int>(g);
     *waves = *grid * v.waves_per_block;
     return W2V_OK;
@@ -642,7 +647,7 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
         W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(v.fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(lds)));
     int grid = 0, waves = 0;
-    if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.workers, a.n_docs, &grid, &waves)) return rc;
+    if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.workers, a.n_units, &grid, &waves)) return rc;
     a.workers = waves;
     if (train_egrad_floats(arch, a.dim, a.stride, window, waves) > 0) {
         if (!a.egrad) return fail(W2V_E_ARG, "internal: egrad rows missing");

@@ -134,6 +134,11 @@ int launch_alpha_table(const w2v_params *p, int64_t blk0, int64_t nblk, float *t
 
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Work units of the training kernels: a document's kept centres in segments of kSegLen, so that a
+// small corpus still spreads over the whole GPU (windows still read the whole document).
+constexpr int kSegLen = 128;
+inline int32_t segs_per_doc(int32_t doc_len) { return static_cast<int32_t>(ceil_div(doc_len, kSegLen)); }
+
 // Arguments of the asynchronous training kernel.
 struct TrainArgs {
     float *syn0;
@@ -148,6 +153,9 @@ struct TrainArgs {
     const int32_t *doc_kept;
     int64_t n_docs;
     int32_t doc_len;
+    int32_t seg_len;         // work unit: up to seg_len consecutive kept centres of one document
+    int32_t segs_per_doc;    // ceil(doc_len / seg_len); unit u = (document u / segs_per_doc, segment u % segs_per_doc)
+    int64_t n_units;         // n_docs * segs_per_doc
     int64_t first_raw;
     int64_t epoch_base;      // epoch * corpus_tokens
     const float *alpha_tab;
