@@ -170,11 +170,13 @@ typedef struct {
  * a window holds no repeated word). alpha decays linearly with the raw stream
  * position in steps of 10,000 tokens down to 1e-4 alpha0.
  *
- * mode 0: documents are claimed by wavefronts from a queue; the top cache_k
+ * mode 0: segments of up to 128 kept centres of a document are claimed by
+ * wavefronts from a queue (in stream order); the top cache_k
  * inner-node vectors live in each workgroup's LDS and are written back as a
  * change (cached - original) every flush_every centres (§3.2); other rows are
- * updated in HBM with atomic adds of their change. Lock-free: results vary
- * with scheduling, as in the paper's Hogwild setting, except with workers=1.
+ * updated in HBM, by atomic adds of their change or, as write_policy selects,
+ * by stores of the new row. Lock-free: results vary with scheduling, as in
+ * the paper's Hogwild setting, except with workers=1.
  * mode 1: every gradient of a batch of sync_batch consecutive kept centres
  * uses the model at the start of the batch; the sums (exact int64 fixed
  * point) are applied at its end. Deterministic. Synchronises the stream once

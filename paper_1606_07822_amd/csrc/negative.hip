@@ -14,7 +14,7 @@
 // table[r_i >> (32 - L)], r = Philox4x32-10(counter (g lo, g hi, epoch, 1+h),
 // key = seed); one equal to the centre word is dropped.
 //
-// GPU form (one wavefront per centre, whole documents from a queue): the
+// GPU form (one wavefront per centre, 128-centre document segments from a queue): the
 // target rows Y are loaded once per centre and held in registers; the window
 // rows X stream through, each once: its dot products with the targets are
 // reduced four at a time (row j of the reduction holds target 4c+j), the

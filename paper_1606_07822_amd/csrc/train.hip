@@ -1,7 +1,8 @@
 // Asynchronous HS training (Algorithm 1, Cached Skipgram HS), GPU form.
 //
-// Worker = one wavefront. Wavefronts claim whole documents from a queue and
-// walk their kept centre words in order. Per centre v with window words
+// Worker = one wavefront. Wavefronts claim work units from a queue -- segments
+// of up to 128 consecutive kept centres of one document -- and walk their
+// centre words in order (windows still read the whole document). Per centre v with window words
 // w_1..w_P the path of v is walked once, four inner nodes at a time: the
 // four rows are loaded together (the next four are prefetched), every window
 // word in order updates all four (dot, sigmoid, gradient, two axpys), and the
