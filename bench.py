@@ -1,9 +1,9 @@
 """Benchmark: trained words/sec of hierarchical-softmax skip-gram on one MI355X.
 
-One step = the whole path over the synthetic corpus, resident in HBM:
-vocabulary (count, order, remap), Huffman tree (codes, points), one training
-epoch (subsampling, window draws, path walks, top-31 LDS cache), held-out
-log-likelihood. value = in-vocabulary raw tokens of the epoch / step time
+One step = the whole path over the synthetic corpus, resident in HBM: reset
+of the model to the initial vectors (device copy), vocabulary (count, order,
+remap), Huffman tree (codes, points), one training epoch (subsampling,
+window draws, path walks, top-31 LDS cache), held-out log-likelihood. value = in-vocabulary raw tokens of the epoch / step time
 (the classic tool's "words" count, taken before subsampling).
 
 The JSON line also carries the roofline of the training kernel (algorithmic
@@ -113,6 +113,8 @@ def main():
     syn0, syn1 = synth.init_weights(voc.V, w.dim)
     model = w2v.make_model(syn0, syn1, voc, tree, dev)
     del syn0, syn1
+    # every step trains one epoch from the same initial model (a device copy, 2.6 GB at V = 1M, d = 300)
+    init0, init1 = model.syn0.clone(), model.syn1.clone()
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, arch=w.arch, corpus_tokens=w.n_tokens,
                    seed=synth.SEED_TRAIN, cache_k=args.cache_k, flush_every=args.flush_every,
                    flush_policy=args.flush_policy, write_policy=args.write_policy, workers=args.workers)
@@ -148,6 +150,8 @@ def main():
     torch.cuda.empty_cache()
 
     def step():
+        model.syn0.copy_(init0)
+        model.syn1.copy_(init1)
         v = w2v.build_vocab(tok, w.vocab, w.min_count)
         t = w2v.build_huffman(v.vocab_counts)
         model.tree = t
@@ -216,7 +220,7 @@ def main():
         "config": {"workload": args.workload, "tokens": w.n_tokens, "vocab_ids": w.vocab, "V": voc.V, "dim": d,
                    "window": w.window, "sample": w.sample, "min_count": w.min_count, "epochs_per_step": 1,
                    "cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
-                   "write_policy": args.write_policy, "step": "vocab + huffman + epoch" +
+                   "write_policy": args.write_policy, "step": "model reset + vocab + huffman + epoch" +
                    ("" if args.no_loglik else " + held-out loglik")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic},
@@ -247,6 +251,7 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
     syn0, _ = synth.init_weights(voc.V, w.dim)
     model = w2v.make_ns_model(syn0, np.zeros((voc.V, w.dim), np.float32), voc, dev)
     del syn0
+    init0, init1 = model.syn0.clone(), model.syn1.clone()
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
                    seed=synth.SEED_TRAIN, negative=K, workers=args.workers)
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL, negative=K)
@@ -269,6 +274,8 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
     torch.cuda.empty_cache()
 
     def step():
+        model.syn0.copy_(init0)
+        model.syn1.copy_(init1)
         v = w2v.build_vocab(tok, w.vocab, w.min_count)
         nz = w2v.build_noise_table(v.vocab_counts)
         model.vocab_counts = v.vocab_counts
@@ -312,7 +319,7 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
         "data": "synthetic (seeded Zipf + topic-mixture corpus standing in for the paper's text corpus)",
         "config": {"workload": args.workload, "tokens": w.n_tokens, "V": voc.V, "dim": w.dim, "window": w.window,
                    "sample": w.sample, "negative": K, "noise_table_entries": int(noise.table.numel()),
-                   "step": "vocab + noise table + epoch" + ("" if args.no_loglik else " + held-out objective")},
+                   "step": "model reset + vocab + noise table + epoch" + ("" if args.no_loglik else " + held-out objective")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": None},
         "train_kernel_ms": kernel_ms,
