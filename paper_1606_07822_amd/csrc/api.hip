@@ -20,8 +20,9 @@ size_t pairs_workspace_bytes(int32_t V, int64_t n_tokens, int32_t doc_len);
 int run_sample_pairs(const int32_t *, int64_t, int32_t, const int64_t *, int64_t, const w2v_params *, int64_t *,
                      int64_t *, int64_t, uint8_t *, int64_t *, int64_t *, uint64_t *, void *, hipStream_t);
 size_t train_lds_bytes(int32_t cache_k, int32_t dim);
-int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_units, int *grid, int *waves);
-int64_t train_egrad_floats(int arch, int dim, int stride, int window, int waves);
+int train_launch_shape(int arch, int dim, int cache_k, bool buf, int workers, int64_t n_units, int *grid,
+                       int *waves);
+int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, int waves);
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals);
 size_t sync_extra_bytes(int32_t V, int32_t dim, int64_t n_docs);
@@ -195,9 +196,11 @@ int64_t egrad_floats(const w2v_model *m, int64_t n_tokens, const w2v_params *p) 
     if (p->mode != 0) return 0;
     int grid = 0, waves = 0;
     const int64_t n_docs = n_tokens > 0 ? ceil_div(n_tokens, static_cast<int64_t>(p->doc_len)) : 0;
-    if (train_launch_shape(p->arch, m->dim, p->cache_k, p->workers, n_docs * segs_per_doc(p->doc_len), &grid, &waves))
+    const bool buf = train_stores_only(p->write_policy, p->cache_k, p->hot_k, m->dim);
+    if (train_launch_shape(p->arch, m->dim, p->cache_k, buf, p->workers, n_docs * segs_per_doc(p->doc_len), &grid,
+                           &waves))
         return 0;
-    return train_egrad_floats(p->arch, m->dim, m->row_stride, p->window, waves);
+    return train_egrad_floats(p->arch, m->dim, buf, m->row_stride, p->window, waves);
 }
 
 size_t train_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
@@ -328,6 +331,7 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     a.flush_every = p->flush_every;
     a.workers = p->workers;
     a.write_policy = p->write_policy;
+    a.stores_only = train_stores_only(p->write_policy, p->cache_k, p->hot_k, m->dim) ? 1 : 0;
     a.flush_scale = p->flush_policy == 1 ? 0.0f : 1.0f;   // 0: set to 1 / workgroups at launch
     a.queue = queue;
     a.stats = tstats;

@@ -195,6 +195,41 @@ __device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainAr
     }
 }
 
+// Buffer-resource row access for the pipelined walk: a row is a raw buffer of dim floats at
+// syn1 + n * stride; an empty range (num_records 0) turns the row's loads into zeros and its
+// stores into no-ops without a branch, so every chunk issues the same memory instructions.
+constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer: no swizzle, 32-bit data
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(float *base, int64_t row, int stride, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(base + row * stride, 0, bytes, kRawBufferWord3);
+}
+
+template <int NE>
+__device__ __forceinline__ void buf_load_row(float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i)
+        r[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (lane + i * kWave) * 4, 0, 0));
+}
+
+template <int NE>
+__device__ __forceinline__ void buf_store_row(const float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i)
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, r[i]), rs, (lane + i * kWave) * 4, 0, 0);
+}
+
+// HBM rows of path nodes c0 .. c0+3; cached rows and rows past the path's end read as zeros.
+template <int NE>
+__device__ __forceinline__ void load_chunk_buf(float (&y)[kChunk][NE], const TrainArgs &a, int my_pt, int c0,
+                                               int len, int lane) {
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+        const int n = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
+        const bool hbm = c0 + j < len && n < a.cache_first;
+        buf_load_row<NE>(y[j], row_rsrc(a.syn1, hbm ? n : 0, a.stride, hbm ? a.dim * 4 : 0), lane);
+    }
+}
+
 // Every input x[0..nx), in order, updates the nc live rows of the chunk held in
 // yc (dot, sigmoid, gradient, then e += g y and y += g x for each row).
 template <int NE, int PG>
@@ -266,8 +301,11 @@ __device__ __forceinline__ void chunk_write_delta(const TrainArgs &a, float *val
 //               stored, need no copy, and those registers hold the prefetched
 //               next chunk instead. With every row stored the whole path is
 //               prefetched.
+//   kPfBuf    : every row is written back by a store; buffer loads and stores with
+//               empty ranges keep each chunk's memory instructions the same, so
+//               the next chunk's loads stay in flight through the compute.
 [[maybe_unused]] constexpr int kPfNone = 0;
-constexpr int kPfAll = 1, kPfSuffix = 2;
+constexpr int kPfAll = 1, kPfSuffix = 2, kPfBuf = 3;
 
 // Walk the path of the centre with the inputs x[0..nx) (in order), accumulating
 // the hidden-layer gradients into e[0..nx). PG = compile-time bound of nx.
@@ -276,6 +314,48 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
                                           float (&e)[PG][NE], int nx, int my_pt, int len, uint64_t code, float alpha,
                                           int lane) {
     float yc[kChunk][NE], y0[kChunk][NE];
+    if constexpr (PF == kPfBuf) {
+        // Every row is written back by a store (HBM rows to HBM, cached rows into the LDS copy):
+        // the pipelined walk. Each chunk issues the same memory instructions -- buffer loads of the
+        // next chunk and buffer stores of this one, with empty ranges where a row is cached or past
+        // the path's end -- so the wait before a chunk's first use counts only the previous chunk's
+        // stores and the next chunk's loads stay in flight during the compute.
+        // the copy of the prefetched rows sits at the end of the loop body, behind this chunk's stores, so
+        // that its wait is counted within one iteration (a wait at the loop head would also have to cover
+        // the different order of the first chunk's loads)
+        load_chunk_buf<NE>(y0, a, my_pt, 0, len, lane);
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+            for (int i = 0; i < NE; ++i) yc[j][i] = y0[j][i];
+        for (int c0 = 0; c0 < len; c0 += kChunk) {
+            load_chunk_buf<NE>(y0, a, my_pt, c0 + kChunk, len, lane);
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j) {
+                if (c0 + j < len) {
+                    const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
+                    if (n >= a.cache_first)
+                        load_row_lds<NE>(yc[j], val + (n - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
+                }
+            }
+            const int nc = min(kChunk, len - c0);
+            chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j) {
+                const int n = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
+                const bool live = j < nc;
+                if (live && n >= a.cache_first)
+                    store_row_lds<NE>(val + (n - a.cache_first) * lds_stride<NE>(a.dim), yc[j], lane, a.dim);
+                const bool hbm = live && n < a.cache_first;
+                buf_store_row<NE>(yc[j], row_rsrc(a.syn1, hbm ? n : 0, a.stride, hbm ? a.dim * 4 : 0), lane);
+            }
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+                for (int i = 0; i < NE; ++i) yc[j][i] = y0[j][i];
+        }
+        return;
+    }
     if constexpr (PF == kPfAll) {
         float yn[kChunk][NE];
         load_chunk<NE>(yc, a, val, my_pt, 0, len, lane);
@@ -579,13 +659,14 @@ Variant variant(int arch) {
 // Register budget per lane: x and e take 2*PG*NE, the chunk rows 2 (3 with the
 // prefetch) * 4 * NE. Occupancy beats prefetch: at dim 300, 3 waves per SIMD
 // without the prefetch ran 21 % faster than 2 with it.
-Variant pick_variant(int arch, int dim) {
+// buf: every row is written back by a store (train_stores_only), the pipelined walk.
+Variant pick_variant(int arch, int dim, bool buf) {
     const int ne = (dim + kWave - 1) / kWave;
-    if (ne <= 1) return variant<1, 20, 16, kPfAll>(arch);
-    if (ne <= 2) return variant<2, 20, 12, kPfAll>(arch);
-    if (ne <= 4) return variant<4, 10, 12, kPfAll>(arch);
-    if (ne <= 5) return variant<5, 10, 12, kPfSuffix>(arch);
-    if (ne <= 8) return variant<8, 4, 8, kPfSuffix>(arch);
+    if (ne <= 1) return buf ? variant<1, 20, 16, kPfBuf>(arch) : variant<1, 20, 16, kPfAll>(arch);
+    if (ne <= 2) return buf ? variant<2, 20, 12, kPfBuf>(arch) : variant<2, 20, 12, kPfAll>(arch);
+    if (ne <= 4) return buf ? variant<4, 10, 12, kPfBuf>(arch) : variant<4, 10, 12, kPfAll>(arch);
+    if (ne <= 5) return buf ? variant<5, 10, 12, kPfBuf>(arch) : variant<5, 10, 12, kPfSuffix>(arch);
+    if (ne <= 8) return buf ? variant<8, 4, 8, kPfBuf>(arch) : variant<8, 4, 8, kPfSuffix>(arch);
     return variant<16, 2, 8, kPfSuffix>(arch);
 }
 
@@ -607,12 +688,13 @@ __global__ void k_write_stats(const int64_t *totals, const unsigned long long *t
 }  // namespace
 
 size_t train_lds_bytes(int32_t cache_k, int32_t dim) {
-    const Variant v = pick_variant(0, dim);
+    const Variant v = pick_variant(0, dim, false);   // the LDS layout is the same for every path
     return 2ull * cache_k * v.ls(dim) * sizeof(float);
 }
 
-int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_units, int *grid, int *waves) {
-    const Variant v = pick_variant(arch, dim);
+int train_launch_shape(int arch, int dim, int cache_k, bool buf, int workers, int64_t n_units, int *grid,
+                       int *waves) {
+    const Variant v = pick_variant(arch, dim, buf);
     if (workers > 0) {
         *grid = static_cast<int>(ceil_div(workers, v.waves_per_block));
         *waves = workers;
@@ -632,15 +714,15 @@ int train_launch_shape(int arch, int dim, int cache_k, int workers, int64_t n_un
     return W2V_OK;
 }
 
-int64_t train_egrad_floats(int arch, int dim, int stride, int window, int waves) {
-    const Variant v = pick_variant(arch, dim);
+int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, int waves) {
+    const Variant v = pick_variant(arch, dim, buf);
     if (arch != 0 || 2 * window <= v.pg) return 0;
     return static_cast<int64_t>(waves) * 2 * window * stride;
 }
 
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals) {
-    const Variant v = pick_variant(arch, a.dim);
+    const Variant v = pick_variant(arch, a.dim, a.stores_only != 0);
     const size_t lds = 2ull * a.cache_k * v.ls(a.dim) * sizeof(float);
     const int block = v.waves_per_block * kWave;
     a.full_rows = a.stride >= v.ne * kWave ? 1 : 0;
@@ -648,9 +730,10 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
         W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(v.fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(lds)));
     int grid = 0, waves = 0;
-    if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.workers, a.n_units, &grid, &waves)) return rc;
+    if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.stores_only != 0, a.workers, a.n_units, &grid, &waves))
+        return rc;
     a.workers = waves;
-    if (train_egrad_floats(arch, a.dim, a.stride, window, waves) > 0) {
+    if (train_egrad_floats(arch, a.dim, a.stores_only != 0, a.stride, window, waves) > 0) {
         if (!a.egrad) return fail(W2V_E_ARG, "internal: egrad rows missing");
         a.egrad_slots = 2 * window;
     }

@@ -134,6 +134,13 @@ int launch_alpha_table(const w2v_params *p, int64_t blk0, int64_t nblk, float *t
 
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Every inner-node row of the walk is written back by a store: uncached rows to HBM (write_policy bit 0)
+// and cached rows into the workgroup's LDS copy (bit 2, or no cache), with no hot rows taking atomic adds.
+// Dims above 512 columns keep the general walk.
+inline bool train_stores_only(int32_t write_policy, int32_t cache_k, int32_t hot_k, int32_t dim) {
+    return (write_policy & 1) && (cache_k == 0 || (write_policy & 4)) && hot_k == 0 && dim <= 512;
+}
+
 // Work units of the training kernels: a document's kept centres in segments of kSegLen, so that a
 // small corpus still spreads over the whole GPU (windows still read the whole document).
 constexpr int kSegLen = 128;
@@ -165,6 +172,7 @@ struct TrainArgs {
     int32_t workers;
     int32_t write_policy;
     int32_t full_rows;       // row_stride covers the variant's NE*64 columns: whole-row writes
+    int32_t stores_only;     // train_stores_only(): every inner-node row is written back by a store
     float flush_scale;       // fraction of the cached rows' change written back (1 = all of it)
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, node updates
