@@ -185,7 +185,8 @@ typedef struct {
  * Errors: W2V_E_ARG for a bad model/params (V < 2, dim not in 1..1024,
  * window not in 1..10, LDS budget exceeded: 2 cache_k rows of 4-byte floats,
  * a row being dim rounded up to 64, 128, 256, 320 or 512 for dim <= 512 and
- * dim above, ...).
+ * dim above, plus, for dim <= 512, 2 KiB of centre records per wavefront of
+ * a workgroup (16 wavefronts for dim <= 64, 12 for dim <= 320, 8 above), ...).
  * ---------------------------------------------------------------------- */
 size_t w2v_train_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
 int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,

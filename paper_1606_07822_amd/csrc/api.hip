@@ -272,7 +272,8 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     if (p->cache_k > m->V - 1) return fail(W2V_E_ARG, "cache_k must be <= V-1");
     const size_t lds = train_lds_bytes(p->cache_k, m->dim);
     if (lds + 1024 > device_max_lds())
-        return fail(W2V_E_ARG, "cache does not fit LDS: 2 * cache_k rows = " + std::to_string(lds) + " bytes");
+        return fail(W2V_E_ARG, "cache does not fit LDS: 2 * cache_k rows and the centre records take " +
+                                    std::to_string(lds) + " bytes");
     if (int rc = check_ws(workspace, workspace_bytes, train_bytes(m, n_tokens, p))) return rc;
     if (ceil_div(std::max<int64_t>(0, n_tokens), p->doc_len) * segs_per_doc(p->doc_len) > INT32_MAX)
         return fail(W2V_E_ARG, "too many documents for one call: split the stream (first_raw_index)");

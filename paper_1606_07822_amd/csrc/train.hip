@@ -83,20 +83,37 @@ __device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3)
 }
 
 // One wave writes the cache's change back to HBM and re-bases val/orig on the
-// result. LDS rows are ls floats apart (ls >= dim, padding kept at zero).
+// result. LDS rows are ls floats apart (ls >= dim, padding kept at zero). The
+// cache_k * dim elements go kFlushBatch per lane at a time: their atomic adds are
+// all issued before the first returned value is used, so a flush costs a few
+// round trips to memory rather than one per row and column.
+constexpr int kFlushBatch = 16;
+
 __device__ void flush_cache_wave(const TrainArgs &a, float *val, float *orig, int ls, int lane) {
-    for (int s = 0; s < a.cache_k; ++s) {
-        float *g = a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride;
-        float *vs = val + s * ls;
-        float *os = orig + s * ls;
-        for (int col = lane; col < a.dim; col += kWave) {
-            const float c = vs[col];
-            const float d = (c - os[col]) * a.flush_scale;
-            if (d != 0.0f) {
-                const float old = atomicAdd(g + col, d);
-                const float nv = old + d;
-                lds_add(vs + col, nv - c);
-                os[col] = nv;
+    const int n = a.cache_k * a.dim;
+    for (int i0 = 0; i0 < n; i0 += kFlushBatch * kWave) {
+        float c[kFlushBatch], d[kFlushBatch], old[kFlushBatch];
+        int li[kFlushBatch];
+#pragma unroll
+        for (int b = 0; b < kFlushBatch; ++b) {
+            const int i = i0 + b * kWave + lane;
+            const int s = i / a.dim, col = i - s * a.dim;
+            li[b] = s * ls + col;
+            c[b] = 0.0f;
+            d[b] = 0.0f;
+            old[b] = 0.0f;
+            if (i < n) {
+                c[b] = val[li[b]];
+                d[b] = (c[b] - orig[li[b]]) * a.flush_scale;
+                if (d[b] != 0.0f) old[b] = atomicAdd(a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride + col, d[b]);
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < kFlushBatch; ++b) {
+            if (d[b] != 0.0f) {
+                const float nv = old[b] + d[b];
+                lds_add(val + li[b], nv - c[b]);
+                orig[li[b]] = nv;
             }
         }
     }
@@ -120,6 +137,10 @@ constexpr bool pad_lds() { return NE <= 8; }
 
 template <int NE>
 __host__ __device__ __forceinline__ int lds_stride(int dim) { return pad_lds<NE>() ? NE * kWave : dim; }
+
+// Centre records of a segment in LDS (16 bytes per centre and wave), except for the widest rows.
+template <int NE>
+constexpr bool rec_slots() { return NE <= 8; }
 
 template <int NE>
 __device__ __forceinline__ void load_row_lds(float (&r)[NE], const float *p, int lane, int dim) {
@@ -204,18 +225,29 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(float *base, int64_t 
     return __builtin_amdgcn_make_buffer_rsrc(base + row * stride, 0, bytes, kRawBufferWord3);
 }
 
+// The lane's byte offset is passed through an empty asm statement where it is used, so that the
+// element steps (i * 256 bytes) stay constants of each access and become its immediate offset
+// (range-checked like the lane offset) instead of one loop-invariant register per element.
+__device__ __forceinline__ int lane_bytes(int lane) {
+    int b = lane * 4;
+    asm volatile("" : "+v"(b));
+    return b;
+}
+
 template <int NE>
 __device__ __forceinline__ void buf_load_row(float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
+    const int b = lane_bytes(lane);
 #pragma unroll
     for (int i = 0; i < NE; ++i)
-        r[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (lane + i * kWave) * 4, 0, 0));
+        r[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, b + i * kWave * 4, 0, 0));
 }
 
 template <int NE>
 __device__ __forceinline__ void buf_store_row(const float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
+    const int b = lane_bytes(lane);
 #pragma unroll
     for (int i = 0; i < NE; ++i)
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, r[i]), rs, (lane + i * kWave) * 4, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, r[i]), rs, b + i * kWave * 4, 0, 0);
 }
 
 // HBM rows of path nodes c0 .. c0+3; cached rows and rows past the path's end read as zeros.
@@ -227,6 +259,41 @@ __device__ __forceinline__ void load_chunk_buf(float (&y)[kChunk][NE], const Tra
         const int n = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
         const bool hbm = c0 + j < len && n < a.cache_first;
         buf_load_row<NE>(y[j], row_rsrc(a.syn1, hbm ? n : 0, a.stride, hbm ? a.dim * 4 : 0), lane);
+    }
+}
+
+// The window words and the path of centre q of the segment (record r, kept position j0 + q): lane l of wv receives the vocabulary index of the l-th window word, lane l of pt the
+// l-th node of the path (PATH false: none). Lanes past the window or the path read zero through
+// the buffers' range checks, so the loads issue without a branch and stay in flight while the
+// centre before is trained.
+// Record of centre q of the segment starting at kept position j0: vocabulary index, meta, path
+// offset, path length. REC: from the wave's LDS slots; else from the kept and tree arrays (the
+// widest rows leave no LDS for the slots).
+template <bool REC>
+__device__ __forceinline__ int4 centre_record(const TrainArgs &a, const int4 *rec, const int32_t *kv,
+                                              const uint32_t *km, int j0, int q) {
+    if constexpr (REC) {
+        return rec[q];
+    } else {
+        const int v = kv[j0 + q];
+        return make_int4(v, static_cast<int>(km[j0 + q]), a.point_off[v], static_cast<int>(a.codelen[v]));
+    }
+}
+
+template <bool PATH>
+__device__ __forceinline__ void fetch_centre(const TrainArgs &a, int4 r, const int32_t *kv, int nk, int j0, int q,
+                                             int lane, int &wv, int &pt) {
+    const int j = j0 + q;
+    const int eff = static_cast<int>(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(r.y)) >> 16);
+    const int lo = max(0, j - eff), hi = min(nk - 1, j + eff);
+    const int c = lo + lane + ((lo + lane >= j) ? 1 : 0);
+    const auto kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(kv), 0, nk * 4, kRawBufferWord3);
+    wv = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(kr, lane < hi - lo ? c * 4 : nk * 4, 0, 0));
+    if constexpr (PATH) {
+        const int po = __builtin_amdgcn_readfirstlane(r.z), len = __builtin_amdgcn_readfirstlane(r.w);
+        const auto pr = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(a.points) + po, 0, len * 4,
+                                                          kRawBufferWord3);
+        pt = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(pr, lane_bytes(lane), 0, 0));
     }
 }
 
@@ -434,7 +501,10 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     float *orig = lds + a.cache_k * LS;
     __shared__ int s_centres;
     __shared__ int s_lock;
+    constexpr bool kRec = rec_slots<NE>();
+    __shared__ int4 s_rec[kRec ? WPB : 1][kRec ? kSegLen : 1];   // per wave: its current segment's centre records
     const int lane = lane_id();
+    const int wib = static_cast<int>(threadIdx.x / kWave);
     if (threadIdx.x == 0) {
         s_centres = 0;
         s_lock = 0;
@@ -448,7 +518,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     }
     __syncthreads();
 
-    const int gw = blockIdx.x * WPB + static_cast<int>(threadIdx.x / kWave);
+    const int gw = blockIdx.x * WPB + wib;
     uint64_t n_kept = 0, n_pairs = 0, n_nodes = 0;
     if (gw < a.workers) {
         while (true) {
@@ -464,9 +534,32 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
             const int64_t base = static_cast<int64_t>(doc) * a.doc_len;
             const int32_t *kv = a.kept_vid + base;
             const uint32_t *km = a.kept_meta + base;
+            // stage the segment's centre records in the wave's LDS slots: one round of gathers per
+            // segment instead of a chain of dependent loads per centre
+            int4 *rec = s_rec[kRec ? wib : 0];
+            if constexpr (kRec) {
+                for (int q = lane; q < j1 - j0; q += kWave) {
+                    const int v = kv[j0 + q];
+                    rec[q] = make_int4(v, static_cast<int>(km[j0 + q]), a.point_off[v], static_cast<int>(a.codelen[v]));
+                }
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            }
+            int wv_next = 0, pt_next = 0;
+            fetch_centre<ARCH != 2>(a, centre_record<kRec>(a, rec, kv, km, j0, 0), kv, nk, j0, 0, lane, wv_next,
+                                    pt_next);
             for (int j = j0; j < j1; ++j) {
-                const uint32_t meta = km[j];
-                const int v = kv[j];
+                const int4 r = centre_record<kRec>(a, rec, kv, km, j0, j - j0);
+                const int v = __builtin_amdgcn_readfirstlane(r.x);
+                const uint32_t meta = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(r.y));
+                // window words (lane q: the q-th one) and path nodes of this centre, fetched during the
+                // centre before; the next centre's are issued now
+                int wv = wv_next, my_pt = pt_next;
+                asm volatile("" : "+v"(wv), "+v"(my_pt));   // one wait for the fetched values here, none at their uses
+                const int qn = min(j + 1, j1 - 1) - j0;
+                fetch_centre<ARCH != 2>(a, centre_record<kRec>(a, rec, kv, km, j0, qn), kv, nk, j0, qn, lane, wv_next,
+                                        pt_next);
                 const int eff = static_cast<int>(meta >> 16);
                 const int lo = max(0, j - eff), hi = min(nk - 1, j + eff);
                 const int P = hi - lo;   // window words, centre excluded
@@ -474,15 +567,8 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                 if (P > 0) {
                     const int64_t g = a.epoch_base + a.first_raw + base + static_cast<int64_t>(meta & 0xFFFFu);
                     const float alpha = a.alpha_tab[g / 10000 - a.blk0];
-                    // window words: lane q holds the vocabulary index of the q-th one
-                    int wv = 0;
-                    if (lane < P) {
-                        const int c = lo + lane + ((lo + lane >= j) ? 1 : 0);
-                        wv = kv[c];
-                    }
-                    const int len = ARCH == 2 ? 0 : a.codelen[v];
+                    const int len = ARCH == 2 ? 0 : __builtin_amdgcn_readfirstlane(r.w);
                     const uint64_t code = ARCH == 2 ? 0 : a.code[v];
-                    const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
 
                     if constexpr (ARCH == 0) {
                         // groups of PG window words walk the path in turn (one group when P <= PG). With
@@ -498,7 +584,10 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                             for (int p = 0; p < PG; ++p) {
                                 if (p < nx) {
                                     const int w = __builtin_amdgcn_readlane(wv, g0 + p);
-                                    load_row<NE>(x[p], a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
+                                    if constexpr (PF == kPfBuf)
+                                        buf_load_row<NE>(x[p], row_rsrc(a.syn0, w, a.stride, a.dim * 4), lane);
+                                    else
+                                        load_row<NE>(x[p], a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
                                 } else {
                                     zero_row<NE>(x[p]);
                                 }
@@ -647,13 +736,15 @@ struct Variant {
     int ne;   // elements per lane
     int pg;   // window words per path walk (skip-gram)
     int (*ls)(int);
+    int rec_bytes;   // static LDS of the centre records
 };
 
 template <int NE, int PG, int WPB, int PF>
 Variant variant(int arch) {
-    if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE, PG, lds_stride<NE>};
-    if (arch == 2) return Variant{k_train<NE, 1, 2, WPB, PF>, WPB, NE, 1, lds_stride<NE>};
-    return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE, 1, lds_stride<NE>};
+    constexpr int rb = rec_slots<NE>() ? WPB * kSegLen * static_cast<int>(sizeof(int4)) : 0;
+    if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE, PG, lds_stride<NE>, rb};
+    if (arch == 2) return Variant{k_train<NE, 1, 2, WPB, PF>, WPB, NE, 1, lds_stride<NE>, rb};
+    return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE, 1, lds_stride<NE>, rb};
 }
 
 // Register budget per lane: x and e take 2*PG*NE, the chunk rows 2 (3 with the
@@ -689,7 +780,7 @@ __global__ void k_write_stats(const int64_t *totals, const unsigned long long *t
 
 size_t train_lds_bytes(int32_t cache_k, int32_t dim) {
     const Variant v = pick_variant(0, dim, false);   // the LDS layout is the same for every path
-    return 2ull * cache_k * v.ls(dim) * sizeof(float);
+    return 2ull * cache_k * v.ls(dim) * sizeof(float) + static_cast<size_t>(v.rec_bytes);
 }
 
 int train_launch_shape(int arch, int dim, int cache_k, bool buf, int workers, int64_t n_units, int *grid,
