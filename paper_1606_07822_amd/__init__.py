@@ -243,14 +243,16 @@ class Model:
         return self.syn0[:, :self.dim], self.syn1[:, :self.dim]
 
 
-def make_model(syn0_init, syn1_init, vocab: Vocab, tree: Tree, device="cuda") -> Model:
-    """Copy [V, dim] initial weights (numpy or torch) into padded device rows."""
+def make_model(syn0_init, syn1_init, vocab: Vocab, tree: Tree, device="cuda", stride: int | None = None,
+               pad_value: float = 0.0) -> Model:
+    """Copy [V, dim] initial weights (numpy or torch) into device rows of `stride` floats (default
+    padded_stride(dim)); the padding columns hold pad_value."""
     s0 = torch.as_tensor(syn0_init, dtype=torch.float32)
     s1 = torch.as_tensor(syn1_init, dtype=torch.float32)
     V, dim = s0.shape
-    stride = padded_stride(dim)
-    syn0 = torch.zeros(V, stride, dtype=torch.float32, device=device)
-    syn1 = torch.zeros(max(V - 1, 1), stride, dtype=torch.float32, device=device)
+    stride = padded_stride(dim) if stride is None else stride
+    syn0 = torch.full((V, stride), pad_value, dtype=torch.float32, device=device)
+    syn1 = torch.full((max(V - 1, 1), stride), pad_value, dtype=torch.float32, device=device)
     syn0[:, :dim].copy_(s0)
     syn1[:V - 1, :dim].copy_(s1)
     return Model(syn0, syn1, dim, vocab.vocab_counts.contiguous(), vocab.train_words, tree)
@@ -439,16 +441,18 @@ def build_noise_table(vocab_counts: torch.Tensor, log2_size: int | None = None) 
     return Noise(table, L, tot.value)
 
 
-def make_ns_model(syn0_init, syn1_init, vocab: Vocab, device="cuda") -> Model:
-    """[V, dim] input and output vectors in padded device rows (no tree)."""
+def make_ns_model(syn0_init, syn1_init, vocab: Vocab, device="cuda", stride: int | None = None,
+                  pad_value: float = 0.0) -> Model:
+    """[V, dim] input and output vectors in device rows of `stride` floats (default padded_stride(dim);
+    padding columns hold pad_value), no tree."""
     s0 = torch.as_tensor(syn0_init, dtype=torch.float32)
     s1 = torch.as_tensor(syn1_init, dtype=torch.float32)
     V, dim = s0.shape
     if tuple(s1.shape) != (V, dim):
         raise ValueError("output vectors must be [V, dim]")
-    stride = padded_stride(dim)
-    syn0 = torch.zeros(V, stride, dtype=torch.float32, device=device)
-    syn1 = torch.zeros(V, stride, dtype=torch.float32, device=device)
+    stride = padded_stride(dim) if stride is None else stride
+    syn0 = torch.full((V, stride), pad_value, dtype=torch.float32, device=device)
+    syn1 = torch.full((V, stride), pad_value, dtype=torch.float32, device=device)
     syn0[:, :dim].copy_(s0)
     syn1[:, :dim].copy_(s1)
     return Model(syn0, syn1, dim, vocab.vocab_counts.contiguous(), vocab.train_words, None)

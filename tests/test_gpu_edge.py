@@ -1,7 +1,8 @@
 """Degenerate and boundary inputs of the training and evaluation paths on the
 GPU (through the C ABI): empty and fully dropped streams, documents too short
 for a window, the smallest tree (V = 2) and vector size (d = 1), a ragged last
-document, a corpus fed in whole-document chunks, and the widest window.
+document, a corpus fed in whole-document chunks, the widest window, rows
+packed with no padding, and padding columns that hold NaN.
 """
 import numpy as np
 import pytest
@@ -154,3 +155,45 @@ def test_widest_window_and_widest_rows(w2v):
     assert list(st) == list(ost)
     g0, g1 = (t.cpu().numpy() for t in model.vectors())
     assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+# Row strides of dim rounded up to 4 only (no padding past the lanes' last element group): every row
+# access must stop at dim columns, or it reads and writes the next row. write_policy 5 and 1 take the
+# store-only walk (buffer loads/stores) and the general one.
+@pytest.mark.parametrize("dim,wp", [(300, 5), (300, 1), (100, 5), (452, 5), (60, 5)])
+def test_packed_rows_match_oracle(w2v, dim, wp):
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = s.tv[:3000]
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, dim, window=5, sample=1e-3, train_words=s.voc.train_words, corpus_tokens=s.tv.size,
+                       order=1, cache_k=31, flush_every=10)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree, stride=(dim + 3) // 4 * 4)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=31, flush_every=10,
+                   write_policy=wp)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+# Padding columns are ignored: NaN there leaves the trained columns bit for bit as with zeros.
+@pytest.mark.parametrize("wp,arch", [(5, 0), (1, 0), (5, 1), (5, 2)])
+def test_padding_contents_are_ignored(w2v, wp, arch):
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = to_dev(s.tv[:4000])
+    syn0, syn1 = synth.init_weights(s.voc.V, 300, syn1_scale=0.5 / 300)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=31, flush_every=10,
+                   write_policy=wp, arch=arch)
+    out = []
+    for pad in (0.0, float("nan")):
+        model = w2v.make_model(syn0, syn1, voc, tree, pad_value=pad)
+        w2v.train_hs_epoch(model, tv, p)
+        out.append([t.cpu().numpy() for t in model.vectors()])
+    for a, b in zip(*out):
+        np.testing.assert_array_equal(a, b)

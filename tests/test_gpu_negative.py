@@ -116,6 +116,32 @@ def test_single_worker_matches_oracle(w2v, K, dim, win, docs, wp):
     np.testing.assert_array_equal(g1[(a1 == syn1).all(1)], syn1[(a1 == syn1).all(1)])
 
 
+# Rows packed with no padding (stride = dim rounded up to 4), and NaN in the padding columns of padded rows.
+@pytest.mark.parametrize("dim,wp,packed", [(300, 3, True), (300, 0, True), (100, 3, True), (300, 3, False),
+                                           (450, 3, False)])
+def test_row_layouts(w2v, dim, wp, packed):
+    s = oracle_side("sg_v30k_d100")
+    tv = s.tv[:3000]
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    L = w2v.noise_log2_size(s.voc.V)
+    noise = w2v.build_noise_table(voc.vocab_counts, L)
+    table = oracle.noise_table(s.voc.vocab_counts, L)
+    rng = np.random.default_rng(dim)
+    syn0 = ((rng.random((s.voc.V, dim)) - 0.5) / dim).astype(np.float32)
+    syn1 = ((rng.random((s.voc.V, dim)) - 0.5) * (1.0 / dim)).astype(np.float32)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, dim, window=5, sample=1e-3, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, negative=5)
+    ost = oracle.train_ns(a0, a1, s.voc.vocab_counts, table, L, tv, op)
+    kw = dict(stride=(dim + 3) // 4 * 4) if packed else dict(pad_value=float("nan"))
+    model = w2v.make_ns_model(syn0, syn1, voc, **kw)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, negative=5, workers=1, write_policy=wp)
+    st = w2v.train_ns_epoch(model, noise, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1, a1) <= 1e-4
+
+
 def test_objective_matches_oracle_on_the_same_model(w2v):
     s = oracle_side("sg_v30k_d100")
     voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
