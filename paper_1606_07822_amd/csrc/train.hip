@@ -817,7 +817,7 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
     const size_t lds = 2ull * a.cache_k * v.ls(a.dim) * sizeof(float);
     const int block = v.waves_per_block * kWave;
     a.full_rows = a.stride >= v.ne * kWave ? 1 : 0;
-    if (lds > 64 * 1024)
+    if (lds + v.rec_bytes > 64 * 1024)   // static (records) plus dynamic (cache) LDS above the default limit
         W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(v.fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(lds)));
     int grid = 0, waves = 0;

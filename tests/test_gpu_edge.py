@@ -197,3 +197,30 @@ def test_padding_contents_are_ignored(w2v, wp, arch):
         out.append([t.cpu().numpy() for t in model.vectors()])
     for a, b in zip(*out):
         np.testing.assert_array_equal(a, b)
+
+
+# Cache sizes around the LDS budget at dim 300 (12 wavefronts of centre records, 24 KiB, plus 2 * k rows of
+# 320 floats): k = 20 crosses the 64 KiB default launch limit only with the records counted, k = 54 is the
+# largest that fits, k = 55 is refused.
+@pytest.mark.parametrize("k", [20, 54, 55])
+def test_cache_sizes_around_the_lds_budget(w2v, k):
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = s.tv[:2000]
+    syn0, syn1 = synth.init_weights(s.voc.V, 300, syn1_scale=0.5 / 300)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=k, flush_every=10)
+    if k == 55:
+        with pytest.raises(w2v.W2VError) as e:
+            w2v.train_hs_epoch(model, to_dev(tv), p)
+        assert e.value.code == w2v.W2V_E_ARG and "LDS" in str(e.value)
+        return
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, 300, window=5, sample=1e-3, train_words=s.voc.train_words, corpus_tokens=s.tv.size,
+                       order=1, cache_k=k, flush_every=10)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
