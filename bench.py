@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--cache-k", type=int, default=31)
     ap.add_argument("--flush-every", type=int, default=1000)
     ap.add_argument("--flush-policy", type=int, default=1)
-    ap.add_argument("--write-policy", type=int, default=5)
+    ap.add_argument("--write-policy", type=int, default=7)
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
     ap.add_argument("--no-probe", action="store_true", help="skip the random-row memory probe")
@@ -189,11 +189,15 @@ def main():
     byte_total = (8 * d * node_rows + 8 * d * pairs + 4 * path_len + 9 * centres
                   + n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k)
     achieved = byte_total / (kernel_ms / 1e3) / 1e9
+    res = w2v.last_train_resources()
+    cfg_keys = {"cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
+                "write_policy": args.write_policy}
     traffic = None
     tfile = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
     if os.path.exists(tfile):
+        # counters taken on this kernel source and these settings only
         t = json.load(open(tfile))
-        if t.get("kernel_source") == w2v.kernel_source_hash():
+        if t.get("kernel_source") == w2v.kernel_source_hash() and t.get("settings") == cfg_keys:
             traffic = t.get("hbm_bytes_per_launch")
 
     # the training kernel moves whole padded rows (row_stride >= 64 * ceil(d / 64) floats) when it can
@@ -234,7 +238,7 @@ def main():
         "memory_probe": probe,
         "counter_calibration": calib,
         "kernel_source": w2v.kernel_source_hash(),
-        "launch": {"workgroups": n_groups, "wavefronts": n_waves},
+        "launch": {"workgroups": n_groups, "wavefronts": n_waves, **res},
     }
     print(json.dumps(line), flush=True)
 
@@ -303,6 +307,7 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
     kernel_ms = sum(kms_all) / len(kms_all)
     achieved = byte_total / (kernel_ms / 1e3) / 1e9
     n_groups, n_waves = w2v.last_train_launch()
+    res = w2v.last_train_resources()
     cpu = None if args.no_cpu_baseline else cpu_baseline_ns(w, tok_np, args, K)
     line = {
         "metric": f"trained words/sec, skip-gram with {K} shared negatives V=1M d=300 fp32; % of HBM roofline",
@@ -329,7 +334,7 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
         "algorithmic_bytes_per_launch": byte_total,
         "heldout_mean_objective": (objs[-1][0] / objs[-1][1]) if objs and objs[-1] else None,
         "cpu_baseline": cpu,
-        "launch": {"workgroups": n_groups, "wavefronts": n_waves},
+        "launch": {"workgroups": n_groups, "wavefronts": n_waves, **res},
     }
     print(json.dumps(line), flush=True)
 

@@ -202,6 +202,15 @@ int w2v_last_train_kernel_ms(float *ms_host);
    (cache owners) and wavefronts that took documents. Host-side, no wait. */
 int w2v_last_train_launch(int32_t *workgroups_host, int32_t *wavefronts_host);
 
+/* Resources of that same launch (the last asynchronous hierarchical-softmax
+   or negative-sampling training kernel on the calling thread's current
+   device): LDS bytes per workgroup (static centre records plus the dynamic
+   cache rows), vector registers per lane as the HIP runtime reports them,
+   and resident wavefronts per SIMD at that LDS size (occupancy). All three
+   are 0 before the first launch. Host-side, no wait. Errors: W2V_E_ARG for a
+   NULL pointer. */
+int w2v_last_train_resources(int32_t *lds_bytes_host, int32_t *vgprs_host, int32_t *waves_per_simd_host);
+
 /* ------------------------------------------------------------------------
  * Hierarchical-softmax log-likelihood (evaluation): over the (centre,
  * context) pairs that the sampler draws from tokens with p's seed, epoch,

@@ -283,7 +283,7 @@ class Params:
     flush_every: int = 1000
     sync_batch: int = 4096
     workers: int = 0
-    write_policy: int = 5
+    write_policy: int = 7
     flush_policy: int = 1
     hot_k: int | None = None
     negative: int = 5
@@ -339,6 +339,14 @@ def last_train_launch() -> tuple[int, int]:
     wv = ctypes.c_int32(0)
     _check(lib().w2v_last_train_launch(ctypes.byref(g), ctypes.byref(wv)))
     return g.value, wv.value
+
+
+def last_train_resources() -> dict:
+    """LDS bytes per workgroup, VGPRs per lane and wavefronts per SIMD of the last asynchronous training
+    launch."""
+    lds, vg, occ = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().w2v_last_train_resources(ctypes.byref(lds), ctypes.byref(vg), ctypes.byref(occ)))
+    return {"lds_bytes_per_workgroup": lds.value, "vgprs": vg.value, "waves_per_simd": occ.value}
 
 
 def hs_loglik(model: Model, tokens: torch.Tensor, p: Params):

@@ -68,6 +68,7 @@ struct DevInfo {
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     bool have_timing = false;
     int last_groups = 0, last_waves = 0;
+    int last_lds = 0, last_vgprs = 0, last_waves_per_simd = 0;
 };
 std::mutex g_mu;
 DevInfo g_dev[64];
@@ -93,11 +94,21 @@ DevInfo &dev_info() {
 }
 
 int device_cu_count() { return dev_info().cus; }
-void record_train_launch(int groups, int waves) {
+void record_train_launch(int groups, int waves, const void *fn, int block, size_t dyn_lds) {
+    hipFuncAttributes fa{};
+    int lds = 0, vgprs = 0, per_cu = 0;
+    if (hipFuncGetAttributes(&fa, fn) == hipSuccess) {
+        lds = static_cast<int>(fa.sharedSizeBytes + dyn_lds);
+        vgprs = fa.numRegs;
+    }
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, block, dyn_lds) != hipSuccess) per_cu = 0;
     DevInfo &di = dev_info();
     std::lock_guard<std::mutex> lk(g_mu);
     di.last_groups = groups;
     di.last_waves = waves;
+    di.last_lds = lds;
+    di.last_vgprs = vgprs;
+    di.last_waves_per_simd = per_cu * (block / kWave) / 4;   // 4 SIMDs per compute unit
 }
 size_t device_max_lds() { return dev_info().lds; }
 
@@ -359,6 +370,17 @@ int w2v_last_train_launch(int32_t *workgroups_host, int32_t *wavefronts_host) {
     std::lock_guard<std::mutex> lk(g_mu);
     *workgroups_host = di.last_groups;
     *wavefronts_host = di.last_waves;
+    return W2V_OK;
+}
+
+int w2v_last_train_resources(int32_t *lds_bytes_host, int32_t *vgprs_host, int32_t *waves_per_simd_host) {
+    g_err.clear();
+    if (!lds_bytes_host || !vgprs_host || !waves_per_simd_host) return fail(W2V_E_ARG, "a required pointer is NULL");
+    DevInfo &di = dev_info();
+    std::lock_guard<std::mutex> lk(g_mu);
+    *lds_bytes_host = di.last_lds;
+    *vgprs_host = di.last_vgprs;
+    *waves_per_simd_host = di.last_waves_per_simd;
     return W2V_OK;
 }
 

@@ -622,7 +622,7 @@ int launch_train_ns(const w2v_model *m, const int32_t *table, int32_t log2_size,
     constexpr int kMinUnits = 8;
     grid = std::max<int64_t>(1, std::min<int64_t>(grid, ceil_div(a.n_units, int64_t(kNsWaves) * kMinUnits)));
     a.workers = p->workers > 0 ? p->workers : static_cast<int32_t>(grid * kNsWaves);
-    record_train_launch(static_cast<int>(grid), a.workers);
+    record_train_launch(static_cast<int>(grid), a.workers, reinterpret_cast<const void *>(fn), kNsWaves * kWave, 0);
     k_zero_ns<<<1, 64, 0, s>>>(a.queue, a.stats);
     W2V_LAUNCH_CHECK("k_zero_ns");
     if (ev0) W2V_HIP(hipEventRecord(ev0, s));

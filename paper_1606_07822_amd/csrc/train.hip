@@ -829,7 +829,7 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
         a.egrad_slots = 2 * window;
     }
     if (a.flush_scale <= 0.0f) a.flush_scale = 1.0f / static_cast<float>(grid);
-    record_train_launch(grid, a.workers);
+    record_train_launch(grid, a.workers, reinterpret_cast<const void *>(v.fn), block, lds);
     k_zero_train<<<1, 64, 0, s>>>(a.queue, a.stats);
     W2V_LAUNCH_CHECK("k_zero_train");
     if (ev0) W2V_HIP(hipEventRecord(ev0, s));

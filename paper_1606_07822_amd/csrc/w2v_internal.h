@@ -46,7 +46,8 @@ struct Carve {
 
 int device_cu_count();
 size_t device_max_lds();
-void record_train_launch(int groups, int waves);
+// Launch shape and resources of a training kernel launch, for w2v_last_train_launch / _resources.
+void record_train_launch(int groups, int waves, const void *fn, int block, size_t dyn_lds);
 
 // ----------------------------------------------------------- device helpers
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): counter (c0..c3), key (k0, k1).

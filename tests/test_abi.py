@@ -223,3 +223,10 @@ def test_noise_table_and_objective_argument_errors(w2v):
     assert lib.w2v_sample_negatives(fake, 100, 10, fake, 100, ctypes.byref(p), None, 10, None, 0, ctypes.byref(n),
                                     ctypes.byref(ctypes.c_uint64(0)), fake, 1 << 30, None) == w2v.W2V_E_ARG
     assert "noise_table" in w2v.last_error()
+
+
+def test_launch_reports_need_pointers(w2v):
+    L = w2v.lib()
+    a, b, c = ctypes.c_int32(-1), ctypes.c_int32(-1), ctypes.c_int32(-1)
+    assert L.w2v_last_train_launch(None, ctypes.byref(b)) == w2v.W2V_E_ARG
+    assert L.w2v_last_train_resources(ctypes.byref(a), None, ctypes.byref(c)) == w2v.W2V_E_ARG

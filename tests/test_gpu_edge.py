@@ -224,3 +224,14 @@ def test_cache_sizes_around_the_lds_budget(w2v, k):
     assert list(st) == list(ost)
     g0, g1 = (t.cpu().numpy() for t in model.vectors())
     assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+def test_launch_resources_are_reported(w2v):
+    s = oracle_side("sg_v30k_d100")
+    voc, tree, syn0, syn1 = tiny_model(w2v, s, dim=300)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    w2v.train_hs_epoch(model, to_dev(s.tv[:20000]), w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size))
+    r = w2v.last_train_resources()
+    # dim 300: 12 wavefronts of 2 KiB records plus 2 * 31 cached rows of 320 floats
+    assert r["lds_bytes_per_workgroup"] >= 12 * 2048 + 2 * 31 * 320 * 4
+    assert 0 < r["vgprs"] <= 512 and 1 <= r["waves_per_simd"] <= 8
