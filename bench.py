@@ -42,7 +42,8 @@ def parse():
     ap.add_argument("--cache-k", type=int, default=31)
     ap.add_argument("--flush-every", type=int, default=1000)
     ap.add_argument("--flush-policy", type=int, default=1)
-    ap.add_argument("--write-policy", type=int, default=7)
+    ap.add_argument("--write-policy", type=int, default=None,
+                    help="default 7 (every row stored); with --ns, 1 (target rows stored, word rows added)")
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
     ap.add_argument("--no-probe", action="store_true", help="skip the random-row memory probe")
@@ -56,7 +57,10 @@ def parse():
     ap.add_argument("--sweep-f", default="1,10,100,1000")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first write, then read, 1.28 GB of rows once each (reference dispatches for HBM byte counters)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.write_policy is None:
+        args.write_policy = 1 if args.ns else 7
+    return args
 
 
 def log(msg):
@@ -257,7 +261,7 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
     del syn0
     init0, init1 = model.syn0.clone(), model.syn1.clone()
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
-                   seed=synth.SEED_TRAIN, negative=K, workers=args.workers)
+                   seed=synth.SEED_TRAIN, negative=K, workers=args.workers, write_policy=args.write_policy)
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL, negative=K)
     held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
     stats = torch.zeros(w2v.N_STATS, dtype=torch.int64, device=dev)
@@ -324,6 +328,7 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
         "data": "synthetic (seeded Zipf + topic-mixture corpus standing in for the paper's text corpus)",
         "config": {"workload": args.workload, "tokens": w.n_tokens, "V": voc.V, "dim": w.dim, "window": w.window,
                    "sample": w.sample, "negative": K, "noise_table_entries": int(noise.table.numel()),
+                   "write_policy": args.write_policy,
                    "step": "model reset + vocab + noise table + epoch" + ("" if args.no_loglik else " + held-out objective")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": None},
