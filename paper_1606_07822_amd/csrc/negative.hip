@@ -177,6 +177,13 @@ __device__ __forceinline__ float dot_partial(const float (&x)[NE], const float (
     return s;
 }
 
+// Partial dot product with target slot t, zero for the padding slots of the last group of four.
+template <int NE, int NT>
+__device__ __forceinline__ float dot_slot(const float (&x)[NE], const float (&y)[NT][NE], int t) {
+    if (t < NT) return dot_partial<NE>(x, y[t]);
+    return 0.0f;
+}
+
 __device__ __forceinline__ float bcast(float v, int lane) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
 }
@@ -258,36 +265,46 @@ __global__ __launch_bounds__(kNsWaves *kWave) void k_train_ns(NsArgs a) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const int n = __builtin_amdgcn_readlane(tg, t);
-                if (n >= 0) load_row<NE>(y[t], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
-                else {
-#pragma unroll
-                    for (int i = 0; i < NE; ++i) y[t][i] = 0.0f;
-                }
+                buf_load_row<NE>(y[t], row_rsrc(a.syn1, n >= 0 ? n : 0, a.stride, n >= 0 ? a.dim * 4 : 0), lane);
 #pragma unroll
                 for (int i = 0; i < NE; ++i) dy[t][i] = 0.0f;
             }
-            // pass 1: gradients of every (window word, target), the targets' change
+            // pass 1: gradients of every (window word, target), the targets' change. Window rows alternate
+            // between two register sets, each loaded one row ahead of its use (empty ranges past the
+            // window), so that a row's load is in flight while the row before it is used.
             const int row = lane >> 4;
-            for (int p = 0; p < P; ++p) {
-                const int w = __builtin_amdgcn_readlane(wv, p);
-                float x[NE];
-                load_row<NE>(x, a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
+            auto step = [&](const float(&x)[NE], int p) {
 #pragma unroll
-                for (int c = 0; c < NT / 4; ++c) {
-                    const float z = reduce4(dot_partial<NE>(x, y[4 * c]), dot_partial<NE>(x, y[4 * c + 1]),
-                                            dot_partial<NE>(x, y[4 * c + 2]), dot_partial<NE>(x, y[4 * c + 3]));
+                for (int c = 0; c < (NT + 3) / 4; ++c) {
+                    const float z = reduce4(dot_slot<NE, NT>(x, y, 4 * c), dot_slot<NE, NT>(x, y, 4 * c + 1),
+                                            dot_slot<NE, NT>(x, y, 4 * c + 2), dot_slot<NE, NT>(x, y, 4 * c + 3));
                     const int t = 4 * c + row;
                     const float label = (t == 0) ? 1.0f : 0.0f;
                     const float f = __builtin_amdgcn_rcpf(1.0f + __expf(-z));
                     const float g = ((tmask >> t) & 1ull) ? (label - f) * alpha : 0.0f;
-                    if ((lane & 15) == 0) G[p * NT + t] = g;
+                    if ((lane & 15) == 0 && t < NT) G[p * NT + t] = g;
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj) {
-                        const float gj = bcast(g, 16 * jj);
+                        if (4 * c + jj < NT) {
+                            const float gj = bcast(g, 16 * jj);
 #pragma unroll
-                        for (int i = 0; i < NE; ++i) dy[4 * c + jj][i] = fmaf(gj, x[i], dy[4 * c + jj][i]);
+                            for (int i = 0; i < NE; ++i) dy[4 * c + jj][i] = fmaf(gj, x[i], dy[4 * c + jj][i]);
+                        }
                     }
                 }
+            };
+            auto window_row = [&](int p) {
+                const bool in = p < P;
+                const int w = __builtin_amdgcn_readlane(wv, min(p, kWave - 1));
+                return row_rsrc(a.syn0, in ? w : 0, a.stride, in ? a.dim * 4 : 0);
+            };
+            float xa[NE], xb[NE];
+            buf_load_row<NE>(xa, window_row(0), lane);
+            for (int p = 0; p < P; p += 2) {
+                buf_load_row<NE>(xb, window_row(p + 1), lane);
+                step(xa, p);
+                buf_load_row<NE>(xa, window_row(p + 2), lane);
+                if (p + 1 < P) step(xb, p + 1);
             }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_wave_barrier();
@@ -399,11 +416,11 @@ __global__ __launch_bounds__(256) void k_ns_objective(NsArgs a) {
                 float x[NE];
                 load_row<NE>(x, a.syn0 + static_cast<int64_t>(w) * a.stride, lane, a.dim);
 #pragma unroll
-                for (int c = 0; c < NT / 4; ++c) {
-                    const float z = reduce4(dot_partial<NE>(x, y[4 * c]), dot_partial<NE>(x, y[4 * c + 1]),
-                                            dot_partial<NE>(x, y[4 * c + 2]), dot_partial<NE>(x, y[4 * c + 3]));
+                for (int c = 0; c < (NT + 3) / 4; ++c) {
+                    const float z = reduce4(dot_slot<NE, NT>(x, y, 4 * c), dot_slot<NE, NT>(x, y, 4 * c + 1),
+                                            dot_slot<NE, NT>(x, y, 4 * c + 2), dot_slot<NE, NT>(x, y, 4 * c + 3));
                     const int t = 4 * c + row;
-                    if ((lane & 15) == 0 && ((tmask >> t) & 1ull)) {
+                    if ((lane & 15) == 0 && t < NT && ((tmask >> t) & 1ull)) {
                         const double u = t == 0 ? static_cast<double>(z) : -static_cast<double>(z);
                         acc += log_sigmoid(u);
                     }
@@ -535,6 +552,7 @@ NsFn pick_by_ne(int ne, bool objective) {
 NsFn pick_ns(int dim, int negative, bool objective) {
     const int ne = (dim + kWave - 1) / kWave;
     if (negative + 1 <= 4) return pick_by_ne<4>(ne, objective);
+    if (negative + 1 <= 6) return pick_by_ne<6>(ne, objective);
     if (negative + 1 <= 8) return pick_by_ne<8>(ne, objective);
     return pick_by_ne<12>(ne, objective);
 }

@@ -216,40 +216,6 @@ __device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainAr
     }
 }
 
-// Buffer-resource row access for the pipelined walk: a row is a raw buffer of dim floats at
-// syn1 + n * stride; an empty range (num_records 0) turns the row's loads into zeros and its
-// stores into no-ops without a branch, so every chunk issues the same memory instructions.
-constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer: no swizzle, 32-bit data
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(float *base, int64_t row, int stride, int bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(base + row * stride, 0, bytes, kRawBufferWord3);
-}
-
-// The lane's byte offset is passed through an empty asm statement where it is used, so that the
-// element steps (i * 256 bytes) stay constants of each access and become its immediate offset
-// (range-checked like the lane offset) instead of one loop-invariant register per element.
-__device__ __forceinline__ int lane_bytes(int lane) {
-    int b = lane * 4;
-    asm volatile("" : "+v"(b));
-    return b;
-}
-
-template <int NE>
-__device__ __forceinline__ void buf_load_row(float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
-    const int b = lane_bytes(lane);
-#pragma unroll
-    for (int i = 0; i < NE; ++i)
-        r[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, b + i * kWave * 4, 0, 0));
-}
-
-template <int NE>
-__device__ __forceinline__ void buf_store_row(const float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
-    const int b = lane_bytes(lane);
-#pragma unroll
-    for (int i = 0; i < NE; ++i)
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, r[i]), rs, b + i * kWave * 4, 0, 0);
-}
-
 // HBM rows of path nodes c0 .. c0+3; cached rows and rows past the path's end read as zeros.
 template <int NE>
 __device__ __forceinline__ void load_chunk_buf(float (&y)[kChunk][NE], const TrainArgs &a, int my_pt, int c0,

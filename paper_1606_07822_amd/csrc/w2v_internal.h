@@ -90,6 +90,41 @@ __device__ __forceinline__ uint64_t fmix64(uint64_t k) {
 
 __device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x & (kWave - 1)); }
 
+// Buffer-resource row access: a row is a raw buffer of dim floats at base + row * stride; columns
+// past dim read as zeros and are not written, and an empty range (num_records 0) turns the row's
+// loads into zeros and its stores into no-ops, so a loop can issue the same memory instructions
+// every iteration without a branch.
+constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer: no swizzle, 32-bit data
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(float *base, int64_t row, int stride, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(base + row * stride, 0, bytes, kRawBufferWord3);
+}
+
+// The lane's byte offset is passed through an empty asm statement where it is used, so that the
+// element steps (i * 256 bytes) stay constants of each access and become its immediate offset
+// (range-checked like the lane offset) instead of one loop-invariant register per element.
+__device__ __forceinline__ int lane_bytes(int lane) {
+    int b = lane * 4;
+    asm volatile("" : "+v"(b));
+    return b;
+}
+
+template <int NE>
+__device__ __forceinline__ void buf_load_row(float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
+    const int b = lane_bytes(lane);
+#pragma unroll
+    for (int i = 0; i < NE; ++i)
+        r[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, b + i * kWave * 4, 0, 0));
+}
+
+template <int NE>
+__device__ __forceinline__ void buf_store_row(const float (&r)[NE], __amdgpu_buffer_rsrc_t rs, int lane) {
+    const int b = lane_bytes(lane);
+#pragma unroll
+    for (int i = 0; i < NE; ++i)
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, r[i]), rs, b + i * kWave * 4, 0, 0);
+}
+
 // Full-wave sum, result in every lane.
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
