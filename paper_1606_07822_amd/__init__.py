@@ -283,7 +283,7 @@ class Params:
     flush_every: int = 1000
     sync_batch: int = 4096
     workers: int = 0
-    write_policy: int = 7
+    write_policy: int = 5
     flush_policy: int = 1
     hot_k: int | None = None
     negative: int = 5

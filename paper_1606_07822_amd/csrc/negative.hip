@@ -124,11 +124,19 @@ __device__ __forceinline__ float dpp_row(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
 }
 
+// Swap the upper 32 lanes of a with the lower 32 lanes of b (permlane32), or the
+// odd rows of a with the even rows of b (permlane16).
 __device__ __forceinline__ void swap32(float &a, float &b) {
-    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
+                                                    false, false);
+    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
+    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
 }
 __device__ __forceinline__ void swap16(float &a, float &b) {
-    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
+                                                    false, false);
+    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
+    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
 }
 
 // Four per-lane partial sums -> row j (lanes 16j..16j+15) holds the 64-lane sum of a_j.

@@ -60,15 +60,18 @@ __device__ __forceinline__ float row_sum(float v) {
 }
 
 // Swap the upper 32 lanes of a with the lower 32 lanes of b (permlane32), or the
-// odd rows of a with the even rows of b (permlane16). Issued as inline assembly:
-// the compiler's builtins for these swaps fold the second result into the first
-// when both are consumed by one expression. The s_nop pairs cover the VALU
-// write-to-read distance the swaps need.
+// odd rows of a with the even rows of b (permlane16).
 __device__ __forceinline__ void swap32(float &a, float &b) {
-    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
+                                                    false, false);
+    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
+    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
 }
 __device__ __forceinline__ void swap16(float &a, float &b) {
-    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
+                                                    false, false);
+    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
+    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
 }
 
 // Four per-lane partial sums -> one register whose row j (lanes 16j..16j+15)

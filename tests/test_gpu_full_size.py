@@ -118,8 +118,9 @@ def test_full_epoch_in_bench_launch(w2v):
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
     s0, npairs, nnodes = w2v.hs_loglik(model, held, pe)
     assert abs(s0 + math.log(2.0) * nnodes) <= 1e-9 * nnodes      # syn1 = 0: every node gives log(1/2)
+    # bench.py's settings: every row stored (write_policy 7)
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
-                   seed=synth.SEED_TRAIN)
+                   seed=synth.SEED_TRAIN, write_policy=7)
     st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
     grid, waves = w2v.last_train_launch()
     log(f"  launch {grid} workgroups, {waves} wavefronts, {w2v.last_train_kernel_ms():.0f} ms")
@@ -190,7 +191,8 @@ def test_full_single_worker_matches_oracle_centre_major(w2v, k, wp):
     np.testing.assert_array_equal(g1[:ov.V - 1][~touched1], syn1[~touched1])
 
 
-def test_full_prefix_async_loglik_within_1pct(w2v):
+@pytest.mark.parametrize("wp", [5, 7])
+def test_full_prefix_async_loglik_within_1pct(w2v, wp):
     g = golden(f"oracle_ll_{NAME}_first{PREFIX}.json")
     w, _, ov, _ = oracle_full()
     assert (g["V"], g["train_words"], g["train_tokens"]) == (ov.V, ov.train_words, PREFIX)
@@ -198,7 +200,8 @@ def test_full_prefix_async_loglik_within_1pct(w2v):
     syn0, syn1 = synth.init_weights(voc.V, w.dim)
     model = w2v.make_model(syn0, syn1, voc, tree)
     del syn0, syn1
-    p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=PREFIX, seed=synth.SEED_TRAIN)
+    p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=PREFIX, seed=synth.SEED_TRAIN,
+                   write_policy=wp)
     st = w2v.train_hs_epoch(model, voc.tokens[:PREFIX], p).cpu().numpy()
     assert list(st) == g["stats"]
     held = to_dev(oracle.remap(corpus(NAME, heldout=True), ov.id_to_vocab))
