@@ -91,8 +91,8 @@ def algorithmic_bytes(torch, voc, tree, mask, doc_len, dim, k, flush_every, n_gr
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this benchmark runs on one GPU only; multi-GPU runs are not part of this build",
-                          "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the training path is single-GPU "
+                                   "(its sharding is a design, not code)", "n_gpus": args.gpus}))
         sys.exit(2)
     import numpy as np
     import torch
