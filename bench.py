@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--cache-k", type=int, default=31)
     ap.add_argument("--flush-every", type=int, default=1000)
     ap.add_argument("--flush-policy", type=int, default=1)
+    ap.add_argument("--cache-mode", type=int, default=0, help="0 = cached copy and original, 1 = delta-only")
     ap.add_argument("--write-policy", type=int, default=None,
                     help="default 7 (every row stored); with --ns, 1 (target rows stored, word rows added)")
     ap.add_argument("--workers", type=int, default=0)
@@ -121,7 +122,8 @@ def main():
     init0, init1 = model.syn0.clone(), model.syn1.clone()
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, arch=w.arch, corpus_tokens=w.n_tokens,
                    seed=synth.SEED_TRAIN, cache_k=args.cache_k, flush_every=args.flush_every,
-                   flush_policy=args.flush_policy, write_policy=args.write_policy, workers=args.workers)
+                   flush_policy=args.flush_policy, write_policy=args.write_policy, workers=args.workers,
+                   cache_mode=args.cache_mode)
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
     # held-out tokens as vocabulary indices (input preparation; the vocabulary is the same every step)
     held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
@@ -195,7 +197,7 @@ def main():
     achieved = byte_total / (kernel_ms / 1e3) / 1e9
     res = w2v.last_train_resources()
     cfg_keys = {"cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
-                "write_policy": args.write_policy}
+                "write_policy": args.write_policy, "cache_mode": args.cache_mode}
     traffic = None
     tfile = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
     if os.path.exists(tfile):
@@ -228,7 +230,8 @@ def main():
         "config": {"workload": args.workload, "tokens": w.n_tokens, "vocab_ids": w.vocab, "V": voc.V, "dim": d,
                    "window": w.window, "sample": w.sample, "min_count": w.min_count, "epochs_per_step": 1,
                    "cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
-                   "write_policy": args.write_policy, "step": "model reset + vocab + huffman + epoch" +
+                   "write_policy": args.write_policy, "cache_mode": args.cache_mode,
+                   "step": "model reset + vocab + huffman + epoch" +
                    ("" if args.no_loglik else " + held-out loglik")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic},
@@ -389,14 +392,20 @@ def sweep_cache(args, torch, w2v, synth, w, voc, tree, model, held, pe, ws, stat
             model.syn1[:voc.V - 1, :w.dim].copy_(s1)
             p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, arch=w.arch, corpus_tokens=w.n_tokens,
                            seed=synth.SEED_TRAIN, cache_k=k, flush_every=f, flush_policy=args.flush_policy,
-                           write_policy=args.write_policy, workers=args.workers)
-            w2v.train_hs_epoch(model, voc.tokens, p, stats=stats, workspace=ws)
+                           write_policy=args.write_policy, workers=args.workers, cache_mode=args.cache_mode)
+            head = {"sweep": "cache_k x flush_every", "workload": args.workload, "cache_k": k, "flush_every": f,
+                    "flush_policy": args.flush_policy, "write_policy": args.write_policy,
+                    "cache_mode": args.cache_mode}
+            try:
+                w2v.train_hs_epoch(model, voc.tokens, p, stats=stats, workspace=ws)
+            except w2v.W2VError as e:   # e.g. a cache that does not fit LDS
+                log(f"k={k} F={f}: {e}")
+                print(json.dumps({**head, "error": str(e)}), flush=True)
+                continue
             kms = w2v.last_train_kernel_ms()
             s, npairs, _ = w2v.hs_loglik(model, held, pe)
             st = stats.cpu().numpy()
-            line = {"sweep": "cache_k x flush_every", "workload": args.workload, "cache_k": k, "flush_every": f,
-                    "flush_policy": args.flush_policy, "write_policy": args.write_policy,
-                    "train_kernel_ms": kms, "words_per_s": int(st[1]) / (kms / 1e3),
+            line = {**head, "train_kernel_ms": kms, "words_per_s": int(st[1]) / (kms / 1e3),
                     "pair_node_updates_per_s": int(st[4]) / (kms / 1e3), "heldout_mean_ll": s / npairs}
             log(f"k={k} F={f}: {kms:.0f} ms, LL {s / npairs:.5f}")
             print(json.dumps(line), flush=True)

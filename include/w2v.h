@@ -147,7 +147,12 @@ typedef struct {
                                 their change; >= 0 */
     int32_t negative;        /* negative sampling (w2v_train_ns_epoch, w2v_ns_objective): negatives per centre,
                                 shared by its window words; 1..11 (1..7 above 320 columns); ignored elsewhere */
-    int32_t reserved2[4];
+    int32_t cache_mode;      /* asynchronous mode's cache: 0 = each workgroup holds a copy of the cached rows and
+                                their values at the last write-back, whose difference it writes back (§3.2);
+                                1 = delta-only: it holds just its change since the last write-back, reads a
+                                cached row as the HBM row plus that change and adds its updates to the change
+                                with LDS atomics (write_policy bit 2 does not apply); half the LDS per row */
+    int32_t reserved2[3];
 } w2v_params;
 
 /* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,
@@ -183,7 +188,8 @@ typedef struct {
  * (to read the number of kept centres).
  * stats: int64[W2V_N_STATS] device buffer, overwritten (may be NULL).
  * Errors: W2V_E_ARG for a bad model/params (V < 2, dim not in 1..1024,
- * window not in 1..10, LDS budget exceeded: 2 cache_k rows of 4-byte floats,
+ * window not in 1..10, cache_mode not 0 or 1, LDS budget exceeded: 2 cache_k
+ * rows (1 with the delta-only cache) of 4-byte floats,
  * a row being dim rounded up to 64, 128, 256, 320 or 512 for dim <= 512 and
  * dim above, plus, for dim <= 512, 2 KiB of centre records per wavefront of
  * a workgroup (16 wavefronts for dim <= 64, 12 for dim <= 320, 8 above), ...).

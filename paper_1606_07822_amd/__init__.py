@@ -45,7 +45,8 @@ class CParams(ctypes.Structure):
                 ("alpha0", ctypes.c_float), ("epoch", I32), ("n_epochs", I32), ("reserved1", I32),
                 ("corpus_tokens", I64), ("first_raw_index", I64), ("seed", U64), ("cache_k", I32),
                 ("flush_every", I32), ("sync_batch", I32), ("workers", I32), ("write_policy", I32),
-                ("flush_policy", I32), ("hot_k", I32), ("negative", I32), ("reserved2", I32 * 4)]
+                ("flush_policy", I32), ("hot_k", I32), ("negative", I32), ("cache_mode", I32),
+                ("reserved2", I32 * 3)]
 
 
 assert ctypes.sizeof(CModel) == 80 and ctypes.sizeof(CParams) == 112
@@ -287,13 +288,14 @@ class Params:
     flush_policy: int = 1
     hot_k: int | None = None
     negative: int = 5
+    cache_mode: int = 0
     extra: dict = field(default_factory=dict)
 
     def c(self) -> CParams:
         return CParams(self.arch, self.mode, self.window, self.doc_len, float(self.sample), float(self.alpha0),
                        self.epoch, self.n_epochs, 0, self.corpus_tokens, self.first_raw_index, self.seed,
                        self.cache_k, self.flush_every, self.sync_batch, self.workers, self.write_policy,
-                       self.flush_policy, self.resolved_hot_k(), self.negative)
+                       self.flush_policy, self.resolved_hot_k(), self.negative, self.cache_mode)
 
     def resolved_hot_k(self) -> int:
         if self.hot_k is not None:

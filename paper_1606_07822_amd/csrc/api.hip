@@ -19,8 +19,8 @@ int run_build_huffman(const int64_t *, int32_t, uint8_t *, uint64_t *, int32_t *
 size_t pairs_workspace_bytes(int32_t V, int64_t n_tokens, int32_t doc_len);
 int run_sample_pairs(const int32_t *, int64_t, int32_t, const int64_t *, int64_t, const w2v_params *, int64_t *,
                      int64_t *, int64_t, uint8_t *, int64_t *, int64_t *, uint64_t *, void *, hipStream_t);
-size_t train_lds_bytes(int32_t cache_k, int32_t dim);
-int train_launch_shape(int arch, int dim, int cache_k, bool buf, int workers, int64_t n_units, int *grid,
+size_t train_lds_bytes(int32_t cache_k, int32_t dim, bool delta);
+int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int workers, int64_t n_units, int *grid,
                        int *waves);
 int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, int waves);
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
@@ -149,6 +149,7 @@ int check_params(const w2v_params *p, bool training) {
         if (p->workers < 0) return fail(W2V_E_ARG, "workers must be >= 0");
         if (p->write_policy < 0 || p->write_policy > 7) return fail(W2V_E_ARG, "write_policy must be in 0..7");
         if (p->flush_policy != 0 && p->flush_policy != 1) return fail(W2V_E_ARG, "flush_policy must be 0 or 1");
+        if (p->cache_mode != 0 && p->cache_mode != 1) return fail(W2V_E_ARG, "cache_mode must be 0 or 1");
         if (p->hot_k < 0) return fail(W2V_E_ARG, "hot_k must be >= 0");
     }
     return W2V_OK;
@@ -203,13 +204,19 @@ __global__ void k_zero_stats(unsigned long long *p) {
 
 // Parked hidden-layer gradients of the asynchronous kernel (skip-gram windows
 // wider than one register group): floats, 0 when none are needed.
+// The write policy the training kernel applies: the delta-only cache updates cached rows by LDS adds.
+int32_t kernel_write_policy(const w2v_params *p) {
+    return (p->cache_mode == 1 && p->cache_k > 0) ? (p->write_policy & ~4) : p->write_policy;
+}
+
 int64_t egrad_floats(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
     if (p->mode != 0) return 0;
     int grid = 0, waves = 0;
     const int64_t n_docs = n_tokens > 0 ? ceil_div(n_tokens, static_cast<int64_t>(p->doc_len)) : 0;
-    const bool buf = train_stores_only(p->write_policy, p->cache_k, p->hot_k, m->dim);
-    if (train_launch_shape(p->arch, m->dim, p->cache_k, buf, p->workers, n_docs * segs_per_doc(p->doc_len), &grid,
-                           &waves))
+    const bool buf = train_stores_only(kernel_write_policy(p), p->cache_k, p->hot_k, m->dim);
+    const bool delta = p->cache_mode == 1 && p->cache_k > 0;
+    if (train_launch_shape(p->arch, m->dim, p->cache_k, delta, buf, p->workers, n_docs * segs_per_doc(p->doc_len),
+                           &grid, &waves))
         return 0;
     return train_egrad_floats(p->arch, m->dim, buf, m->row_stride, p->window, waves);
 }
@@ -281,9 +288,9 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     if (int rc = check_params(p, true)) return rc;
     if (n_tokens < 0 || (n_tokens > 0 && !tokens)) return fail(W2V_E_ARG, "bad tokens / n_tokens");
     if (p->cache_k > m->V - 1) return fail(W2V_E_ARG, "cache_k must be <= V-1");
-    const size_t lds = train_lds_bytes(p->cache_k, m->dim);
+    const size_t lds = train_lds_bytes(p->cache_k, m->dim, p->cache_mode == 1);
     if (lds + 1024 > device_max_lds())
-        return fail(W2V_E_ARG, "cache does not fit LDS: 2 * cache_k rows and the centre records take " +
+        return fail(W2V_E_ARG, "cache does not fit LDS: the cache_k rows and the centre records take " +
                                     std::to_string(lds) + " bytes");
     if (int rc = check_ws(workspace, workspace_bytes, train_bytes(m, n_tokens, p))) return rc;
     if (ceil_div(std::max<int64_t>(0, n_tokens), p->doc_len) * segs_per_doc(p->doc_len) > INT32_MAX)
@@ -342,8 +349,9 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     a.atomic_first = static_cast<int32_t>(std::max<int64_t>(0, static_cast<int64_t>(a.cache_first) - p->hot_k));
     a.flush_every = p->flush_every;
     a.workers = p->workers;
-    a.write_policy = p->write_policy;
-    a.stores_only = train_stores_only(p->write_policy, p->cache_k, p->hot_k, m->dim) ? 1 : 0;
+    a.cache_delta = (p->cache_mode == 1 && p->cache_k > 0) ? 1 : 0;
+    a.write_policy = kernel_write_policy(p);
+    a.stores_only = train_stores_only(a.write_policy, p->cache_k, p->hot_k, m->dim) ? 1 : 0;
     a.flush_scale = p->flush_policy == 1 ? 0.0f : 1.0f;   // 0: set to 1 / workgroups at launch
     a.queue = queue;
     a.stats = tstats;

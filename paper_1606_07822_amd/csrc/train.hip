@@ -94,6 +94,19 @@ constexpr int kFlushBatch = 16;
 
 __device__ void flush_cache_wave(const TrainArgs &a, float *val, float *orig, int ls, int lane) {
     const int n = a.cache_k * a.dim;
+    if (a.cache_delta) {
+        // delta-only cache: add the scaled change to HBM and take the whole of it out of LDS (changes
+        // that other waves add meanwhile stay); the next reads see the HBM row with the written share
+        for (int i = lane; i < n; i += kWave) {
+            const int s = i / a.dim, col = i - s * a.dim;
+            const float d = val[s * ls + col];
+            if (d != 0.0f) {
+                atomicAdd(a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride + col, d * a.flush_scale);
+                lds_add(val + s * ls + col, -d);
+            }
+        }
+        return;
+    }
     for (int i0 = 0; i0 < n; i0 += kFlushBatch * kWave) {
         float c[kFlushBatch], d[kFlushBatch], old[kFlushBatch];
         int li[kFlushBatch];
@@ -210,9 +223,17 @@ __device__ __forceinline__ void load_chunk(float (&y)[kChunk][NE], const TrainAr
     for (int j = 0; j < kChunk; ++j) {
         if (c0 + j < len) {
             const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-            if (n >= a.cache_first)
+            if (n >= a.cache_first && !a.cache_delta) {
                 load_row_lds<NE>(y[j], val + (n - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
-            else load_row<NE>(y[j], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
+            } else {
+                load_row<NE>(y[j], a.syn1 + static_cast<int64_t>(n) * a.stride, lane, a.dim);
+                if (n >= a.cache_first) {   // delta-only cache: the HBM row plus the workgroup's change
+                    float d[NE];
+                    load_row_lds<NE>(d, val + (n - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) y[j][i] += d[i];
+                }
+            }
         } else {
             zero_row<NE>(y[j]);
         }
@@ -480,6 +501,10 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     }
     const int kd = a.cache_k * LS;
     for (int i = threadIdx.x; i < kd; i += blockDim.x) {
+        if (a.cache_delta) {   // delta-only cache: no change yet (and no copy of the original)
+            val[i] = 0.0f;
+            continue;
+        }
         const int s = i / LS, col = i - s * LS;
         const float v = col < a.dim ? a.syn1[static_cast<int64_t>(a.cache_first + s) * a.stride + col] : 0.0f;
         val[i] = v;
@@ -693,7 +718,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     __syncthreads();
     // final write-back of the cache
     for (int i = threadIdx.x; i < kd; i += blockDim.x) {
-        const float d = (val[i] - orig[i]) * a.flush_scale;
+        const float d = (a.cache_delta ? val[i] : val[i] - orig[i]) * a.flush_scale;
         const int s = i / LS, col = i - s * LS;
         if (d != 0.0f && col < a.dim) atomicAdd(a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride + col, d);
     }
@@ -747,12 +772,12 @@ __global__ void k_write_stats(const int64_t *totals, const unsigned long long *t
 
 }  // namespace
 
-size_t train_lds_bytes(int32_t cache_k, int32_t dim) {
+size_t train_lds_bytes(int32_t cache_k, int32_t dim, bool delta) {
     const Variant v = pick_variant(0, dim, false);   // the LDS layout is the same for every path
-    return 2ull * cache_k * v.ls(dim) * sizeof(float) + static_cast<size_t>(v.rec_bytes);
+    return (delta ? 1ull : 2ull) * cache_k * v.ls(dim) * sizeof(float) + static_cast<size_t>(v.rec_bytes);
 }
 
-int train_launch_shape(int arch, int dim, int cache_k, bool buf, int workers, int64_t n_units, int *grid,
+int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int workers, int64_t n_units, int *grid,
                        int *waves) {
     const Variant v = pick_variant(arch, dim, buf);
     if (workers > 0) {
@@ -760,7 +785,7 @@ int train_launch_shape(int arch, int dim, int cache_k, bool buf, int workers, in
         *waves = workers;
         return W2V_OK;
     }
-    const size_t lds = 2ull * cache_k * v.ls(dim) * sizeof(float);
+    const size_t lds = (delta ? 1ull : 2ull) * cache_k * v.ls(dim) * sizeof(float);
     int per_cu = 0;
     W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(v.fn),
                                                          v.waves_per_block * kWave, lds));
@@ -783,14 +808,15 @@ int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, 
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals) {
     const Variant v = pick_variant(arch, a.dim, a.stores_only != 0);
-    const size_t lds = 2ull * a.cache_k * v.ls(a.dim) * sizeof(float);
+    const size_t lds = (a.cache_delta ? 1ull : 2ull) * a.cache_k * v.ls(a.dim) * sizeof(float);
     const int block = v.waves_per_block * kWave;
     a.full_rows = a.stride >= v.ne * kWave ? 1 : 0;
     if (lds + v.rec_bytes > 64 * 1024)   // static (records) plus dynamic (cache) LDS above the default limit
         W2V_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(v.fn), hipFuncAttributeMaxDynamicSharedMemorySize,
                                     static_cast<int>(lds)));
     int grid = 0, waves = 0;
-    if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.stores_only != 0, a.workers, a.n_units, &grid, &waves))
+    if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.cache_delta != 0, a.stores_only != 0, a.workers,
+                                    a.n_units, &grid, &waves))
         return rc;
     a.workers = waves;
     if (train_egrad_floats(arch, a.dim, a.stores_only != 0, a.stride, window, waves) > 0) {

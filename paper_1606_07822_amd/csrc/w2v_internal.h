@@ -210,6 +210,7 @@ struct TrainArgs {
     int32_t full_rows;       // row_stride covers the variant's NE*64 columns: whole-row writes
     int32_t stores_only;     // train_stores_only(): every inner-node row is written back by a store
     float flush_scale;       // fraction of the cached rows' change written back (1 = all of it)
+    int32_t cache_delta;     // delta-only cache: LDS holds the workgroup's change of each cached row only
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, node updates
     float *egrad;            // per wavefront egrad_slots rows of row_stride floats (parked gradients), or null

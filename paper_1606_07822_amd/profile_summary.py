@@ -96,7 +96,8 @@ def traffic(args):
     f_kib, w_kib = float(tf["Counter_Value"]), float(tw["Counter_Value"])
     rd, wt = f_kib * 1024 / read_factor, w_kib * 1024 / write_factor
     ms = (int(tf["End_Timestamp"]) - int(tf["Start_Timestamp"])) / 1e6
-    settings = {k: b["config"][k] for k in ("cache_k", "flush_every", "flush_policy", "write_policy")}
+    settings = {k: b["config"].get(k, 0) for k in ("cache_k", "flush_every", "flush_policy", "write_policy",
+                                                   "cache_mode")}
     res = {"workload": args.workload, "kernel": tf["Kernel_Name"], "kernel_source": _hash(), "settings": settings,
            "fetch_kib_raw": f_kib, "write_kib_raw": w_kib, "read_factor": read_factor, "write_factor": write_factor,
            "hbm_read_bytes_per_launch": rd, "hbm_write_bytes_per_launch": wt, "hbm_bytes_per_launch": rd + wt,

@@ -43,7 +43,7 @@ def test_struct_layouts_match_header(w2v):
     assert w2v.CModel.points.offset == 72 and ctypes.sizeof(w2v.CModel) == 80
     assert w2v.CParams.sample.offset == 16 and w2v.CParams.corpus_tokens.offset == 40
     assert w2v.CParams.seed.offset == 56 and w2v.CParams.write_policy.offset == 80
-    assert w2v.CParams.hot_k.offset == 88
+    assert w2v.CParams.hot_k.offset == 88 and w2v.CParams.cache_mode.offset == 96
     assert ctypes.sizeof(w2v.CParams) == 112
 
 
@@ -117,6 +117,7 @@ def _params(w2v, **kw):
     ({}, dict(hot_k=-1), "hot_k"),
     ({}, dict(write_policy=8), "write_policy"),
     ({}, dict(flush_policy=2), "flush_policy"),
+    ({}, dict(cache_mode=2), "cache_mode"),
 ])
 def test_train_argument_errors(w2v, mk, pk, msg):
     L = w2v.lib()

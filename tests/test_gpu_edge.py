@@ -235,3 +235,40 @@ def test_launch_resources_are_reported(w2v):
     # dim 300: 12 wavefronts of 2 KiB records plus 2 * 31 cached rows of 320 floats
     assert r["lds_bytes_per_workgroup"] >= 12 * 2048 + 2 * 31 * 320 * 4
     assert 0 < r["vgprs"] <= 512 and 1 <= r["waves_per_simd"] <= 8
+
+
+# Delta-only cache (cache_mode 1): LDS holds only the workgroup's change of each cached row, so twice as
+# many rows fit; with one worker it is the same computation as the copy-and-original cache of the oracle.
+@pytest.mark.parametrize("arch,k,dim,wp", [(0, 31, 100, 1), (0, 31, 300, 5), (0, 31, 300, 0), (1, 31, 300, 5),
+                                           (2, 31, 100, 5), (0, 108, 300, 5), (0, 7, 64, 7)])
+def test_delta_only_cache_single_worker_matches_oracle(w2v, arch, k, dim, wp):
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = s.tv[:3000]
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    alpha0 = 0.05 if arch == 1 else 0.025
+    # the reversed orientation is the oracle's pair-major order with its orientation flag
+    order = dict(order=0, orient=1) if arch == 2 else dict(order=1, arch=arch)
+    op = oracle.params(s.voc.V, dim, window=5, sample=1e-3, train_words=s.voc.train_words, corpus_tokens=s.tv.size,
+                       cache_k=k, flush_every=10, alpha0=alpha0, **order)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=k, flush_every=10,
+                   write_policy=wp, arch=arch, alpha0=alpha0, cache_mode=1)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
+def test_delta_only_cache_lds_budget(w2v):
+    # dim 300: 12 x 2 KiB of centre records plus k rows of 320 floats; k = 109 no longer fits
+    s = oracle_side("sg_v30k_d100")
+    voc, tree, syn0, syn1 = tiny_model(w2v, s, dim=300)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=s.tv.size, workers=1, cache_k=109, cache_mode=1)
+    with pytest.raises(w2v.W2VError) as e:
+        w2v.train_hs_epoch(model, to_dev(s.tv[:2000]), p)
+    assert e.value.code == w2v.W2V_E_ARG and "LDS" in str(e.value)

@@ -337,7 +337,7 @@ def golden(name):
 # of the change everywhere (write_policy 0) or in LDS only (1); no cache; and the cache with the paper's
 # summed write-back, which is stable only at low concurrency (256 wavefronts). CBOW's default also adds
 # the change atomically on the 1024 hot rows below the cache. write_policy 7 (word rows stored too) is
-# the benchmark's setting.
+# the benchmark's setting; cache_mode 1 the delta-only cache.
 @pytest.mark.parametrize("name,kw", [
     ("sg_v30k_d100", {}),
     ("sg_v30k_d100", dict(write_policy=7)),
@@ -345,10 +345,13 @@ def golden(name):
     ("sg_v30k_d100", dict(write_policy=1)),
     ("sg_v30k_d100", dict(cache_k=0)),
     ("sg_v30k_d100", dict(workers=256, cache_k=31, flush_every=10, flush_policy=0, write_policy=0)),
+    ("sg_v30k_d100", dict(cache_mode=1)),
+    ("sg_v30k_d100", dict(cache_mode=1, cache_k=63, flush_every=100)),
     ("sg_v100k_d200", {}),
     ("sg_v100k_d200", dict(write_policy=0)),
     ("sg_v100k_d200", dict(write_policy=1)),
     ("sg_v100k_d200", dict(write_policy=7)),
+    ("sg_v100k_d200", dict(cache_mode=1)),
     ("cbow_v100k_d300", {}),
     ("cbow_v100k_d300", dict(write_policy=7)),
 ])
