@@ -92,9 +92,9 @@ __device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3)
 // round trips to memory rather than one per row and column.
 constexpr int kFlushBatch = 16;
 
-__device__ void flush_cache_wave(const TrainArgs &a, float *val, float *orig, int ls, int lane) {
+__device__ void flush_cache_wave(const TrainArgs &a, bool delta, float *val, float *orig, int ls, int lane) {
     const int n = a.cache_k * a.dim;
-    if (a.cache_delta) {
+    if (delta) {
         // delta-only cache: add the scaled change to HBM and take the whole of it out of LDS (changes
         // that other waves add meanwhile stay); the next reads see the HBM row with the written share
         for (int i = lane; i < n; i += kWave) {
@@ -495,13 +495,15 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     __shared__ int4 s_rec[kRec ? WPB : 1][kRec ? kSegLen : 1];   // per wave: its current segment's centre records
     const int lane = lane_id();
     const int wib = static_cast<int>(threadIdx.x / kWave);
+    // the store-only walk never runs with the delta-only cache (its cached rows take LDS adds)
+    const bool delta = PF != kPfBuf && a.cache_delta != 0;
     if (threadIdx.x == 0) {
         s_centres = 0;
         s_lock = 0;
     }
     const int kd = a.cache_k * LS;
     for (int i = threadIdx.x; i < kd; i += blockDim.x) {
-        if (a.cache_delta) {   // delta-only cache: no change yet (and no copy of the original)
+        if (delta) {   // delta-only cache: no change yet (and no copy of the original)
             val[i] = 0.0f;
             continue;
         }
@@ -702,7 +704,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     }
                     go = __builtin_amdgcn_readfirstlane(go);
                     if (go) {
-                        flush_cache_wave(a, val, orig, LS, lane);
+                        flush_cache_wave(a, delta, val, orig, LS, lane);
                         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
                         if (lane == 0) atomicExch(&s_lock, 0);
                     }
@@ -718,7 +720,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     __syncthreads();
     // final write-back of the cache
     for (int i = threadIdx.x; i < kd; i += blockDim.x) {
-        const float d = (a.cache_delta ? val[i] : val[i] - orig[i]) * a.flush_scale;
+        const float d = (delta ? val[i] : val[i] - orig[i]) * a.flush_scale;
         const int s = i / LS, col = i - s * LS;
         if (d != 0.0f && col < a.dim) atomicAdd(a.syn1 + static_cast<int64_t>(a.cache_first + s) * a.stride + col, d);
     }
