@@ -110,6 +110,8 @@ def traffic(args):
            f"  {args.command_fetch}", f"  {args.command_write}"]
     if args.sq:
         out.append(f"  {args.command_sq}")
+    for c in args.command_tcc or []:
+        out.append(f"  {c}")
     out += ["", f"kernel: {tf['Kernel_Name']}", f"  grid {tf['Grid_Size']} threads, workgroup {tf['Workgroup_Size']}, "
             f"arch VGPR {tf['VGPR_Count']}, LDS {tf['LDS_Block_Size']} B", f"  duration under counters: {ms:.1f} ms", "",
             "HBM bytes (fabric side of L2):",
@@ -132,6 +134,21 @@ def traffic(args):
         if "SQ_INSTS_LDS" in vals and vals["SQ_INSTS_LDS"] and "SQ_LDS_BANK_CONFLICT" in vals:
             out.append(f"  LDS bank conflicts per LDS instruction: "
                        f"{vals['SQ_LDS_BANK_CONFLICT'] / vals['SQ_INSTS_LDS']:.4f}")
+    if args.tcc:
+        vals = {}
+        for f in args.tcc:
+            vals.update({r["Counter_Name"]: float(r["Counter_Value"]) for r in _dispatches(f) if "k_train<" in r["Kernel_Name"]})
+        out += ["", "L2 (TCC) counters (sum over the device):"]
+        out += [f"  {k:<36} {v:.4g}" for k, v in sorted(vals.items())]
+        if vals.get("TCC_HIT_sum") and vals.get("TCC_MISS_sum"):
+            h, m = vals["TCC_HIT_sum"], vals["TCC_MISS_sum"]
+            out.append(f"  L2 hit rate: {h / (h + m):.3f}")
+        if vals.get("TCC_EA0_RDREQ_LEVEL_sum") and vals.get("TCC_EA0_RDREQ_sum"):
+            out.append(f"  mean read latency past L2 (queue level / requests): "
+                       f"{vals['TCC_EA0_RDREQ_LEVEL_sum'] / vals['TCC_EA0_RDREQ_sum']:.0f} cycles")
+        if vals.get("TCC_EA0_WRREQ_LEVEL_sum") and vals.get("TCC_EA0_WRREQ_sum"):
+            out.append(f"  mean write latency past L2: "
+                       f"{vals['TCC_EA0_WRREQ_LEVEL_sum'] / vals['TCC_EA0_WRREQ_sum']:.0f} cycles")
     with open(args.out_txt, "w") as fh:
         fh.write("\n".join(out) + "\n")
 
@@ -154,6 +171,8 @@ def main():
     t.add_argument("--calib-fetch", help="FETCH_SIZE csv holding k_probe<2> if not FETCH_CSV")
     t.add_argument("--sq")
     t.add_argument("--command-sq", default="")
+    t.add_argument("--tcc", action="append", help="L2 counter csv (repeatable)")
+    t.add_argument("--command-tcc", action="append")
     args = ap.parse_args()
     stats(args) if args.cmd == "stats" else traffic(args)
 
