@@ -45,7 +45,8 @@ size_t ns_negatives_extra_bytes(int64_t n_docs);
 int run_ns_negatives(const w2v_params *p, const int32_t *table, int32_t log2_size, const SampleBufs &b,
                      int64_t n_tokens, Carve &c, int32_t *out, int64_t cap, int64_t *n_kept_host,
                      uint64_t *checksum_host, hipStream_t s);
-size_t loglik_extra_bytes(int64_t n_docs);
+int64_t loglik_units(int64_t n_tokens, int32_t doc_len);
+size_t loglik_extra_bytes(int64_t n_units);
 int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
                double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, hipStream_t s);
 
@@ -396,7 +397,7 @@ size_t w2v_hs_loglik_workspace_bytes(const w2v_model *m, int64_t n_tokens, const
     if (!m || !p || p->doc_len < 1 || m->V < 2) return 0;
     Carve c;
     sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
-    return c.used() + loglik_extra_bytes(std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len)));
+    return c.used() + loglik_extra_bytes(loglik_units(n_tokens, p->doc_len));
 }
 
 int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,

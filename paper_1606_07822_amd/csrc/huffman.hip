@@ -31,11 +31,21 @@ __device__ __forceinline__ int64_t leaf_val(const int64_t *__restrict__ counts, 
 // is < the leaf front), the block writes the whole run at once: merge a+i takes
 // elements 2i (bit 0) and 2i+1 (bit 1) of that queue. New inner nodes join the back
 // of their queue and never take part in the run that creates them.
+//
+// Lane 0 reads both queues from LDS: each phase starts with the block copying the next
+// kWin leaves and the next kWin inner counts (those created before the phase) into LDS,
+// and the counts lane 0 creates go to a third LDS window as well as to memory. A phase
+// whose merges would reach past a window ends early and the next one refills them.
+constexpr int kWin = 1024;
+
 __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__restrict__ counts, int32_t V,
                                                               int32_t *__restrict__ parent, uint8_t *__restrict__ bit,
                                                               int64_t *__restrict__ icount, int32_t *__restrict__ flags) {
     __shared__ int32_t s_pl, s_ih, s_a, s_mode;
     __shared__ int64_t s_front;
+    __shared__ int64_t s_leaf[kWin];    // leaf values at queue positions [lb, lb + kWin)
+    __shared__ int64_t s_inner[kWin];   // inner counts [ib, ib + kWin), those below a0
+    __shared__ int64_t s_new[kWin];     // inner counts created in this phase: a0, a0 + 1, ...
     const int tid = threadIdx.x;
     if (tid == 0) {
         s_pl = 0;
@@ -45,20 +55,39 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
     __syncthreads();
     const int64_t max_phases = 4LL * V + 16;   // every phase merges at least once
     for (int64_t phase = 0; phase < max_phases; ++phase) {
+        const int32_t lb = s_pl, ib = s_ih, a0 = s_a;
+        for (int i = tid; i < kWin; i += kMergeThreads) {
+            s_leaf[i] = lb + i < V ? leaf_val(counts, V, lb + i) : 0;
+            s_inner[i] = ib + i < a0 ? icount[ib + i] : 0;
+        }
+        __syncthreads();
         if (tid == 0) {
-            int32_t pl = s_pl, ih = s_ih, a = s_a;
-            int mode = 0;   // 0 done, 1 leaf run, 2 inner run
+            int32_t pl = lb, ih = ib, a = a0;
+            int mode = 0;   // 0 done, 1 leaf run, 2 inner run, 3 refill the windows
             int64_t front = 0;
+            // queue values by position / index; callers stay inside the windows (checked below)
+            auto leafv = [&](int32_t q) { return s_leaf[q - lb]; };
+            auto innerv = [&](int32_t q) { return q < a0 ? s_inner[q - ib] : s_new[q - a0]; };
             while (a < V - 1) {
+                // this merge reads leaves pl .. pl+2kRunMin-1 and inner nodes ih .. min(ih+2kRunMin, a)-1 at most,
+                // and writes new count a
+                const int32_t hi = min(ih + 2 * kRunMin, a);
+                const bool leaf_ok = lb + kWin >= V || pl + 2 * kRunMin <= lb + kWin;
+                const bool inner_ok =
+                    min(hi, a0) - ib <= kWin && (hi <= a0 || hi - a0 <= kWin) && a - a0 < kWin;
+                if (!leaf_ok || !inner_ok) {
+                    mode = 3;
+                    break;
+                }
                 const int32_t nl = V - pl, ni = a - ih;
-                const int64_t FI = ni > 0 ? icount[ih] : 0;
-                const int64_t FL = nl > 0 ? leaf_val(counts, V, pl) : 0;
-                if (ni > 0 && nl >= 2 * kRunMin && leaf_val(counts, V, pl + 2 * kRunMin - 1) <= FI) {
+                const int64_t FI = ni > 0 ? innerv(ih) : 0;
+                const int64_t FL = nl > 0 ? leafv(pl) : 0;
+                if (ni > 0 && nl >= 2 * kRunMin && leafv(pl + 2 * kRunMin - 1) <= FI) {
                     mode = 1;
                     front = FI;
                     break;
                 }
-                if (ni >= 2 * kRunMin && (nl == 0 || icount[ih + 2 * kRunMin - 1] < FL)) {
+                if (ni >= 2 * kRunMin && (nl == 0 || innerv(ih + 2 * kRunMin - 1) < FL)) {
                     mode = 2;
                     front = nl > 0 ? FL : INT64_MAX;
                     break;
@@ -67,14 +96,14 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
                 int64_t sum = 0;
 #pragma unroll
                 for (int b = 0; b < 2; ++b) {
-                    const bool use_leaf = pl < V && (ih >= a || leaf_val(counts, V, pl) <= icount[ih]);
+                    const bool use_leaf = pl < V && (ih >= a || leafv(pl) <= innerv(ih));
                     int32_t child;
                     if (use_leaf) {
-                        sum += leaf_val(counts, V, pl);
+                        sum += leafv(pl);
                         child = V - 1 - pl;
                         ++pl;
                     } else {
-                        sum += icount[ih];
+                        sum += innerv(ih);
                         child = V + ih;
                         ++ih;
                     }
@@ -82,6 +111,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
                     bit[child] = static_cast<uint8_t>(b);
                 }
                 icount[a] = sum;
+                s_new[a - a0] = sum;
                 ++a;
             }
             s_pl = pl;
@@ -94,6 +124,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
         __syncthreads();
         const int mode = s_mode;
         if (mode == 0) return;
+        if (mode == 3) continue;   // windows refilled at the top of the next phase
         const int32_t pl = s_pl, ih = s_ih, a = s_a;
         const int64_t front = s_front;
         // length of the run: the queue's elements below the other front form a prefix

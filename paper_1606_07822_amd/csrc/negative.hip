@@ -118,42 +118,6 @@ __device__ __forceinline__ int target_of(int t, int v, int K, uint64_t seed, int
     return n == v ? -1 : n;
 }
 
-// -------------------------------------------------------- cross-lane helpers
-template <int CTRL>
-__device__ __forceinline__ float dpp_row(float v) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
-}
-
-// Swap the upper 32 lanes of a with the lower 32 lanes of b (permlane32), or the
-// odd rows of a with the even rows of b (permlane16).
-__device__ __forceinline__ void swap32(float &a, float &b) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
-                                                    false, false);
-    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
-    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
-}
-__device__ __forceinline__ void swap16(float &a, float &b) {
-    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
-                                                    false, false);
-    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
-    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
-}
-
-// Four per-lane partial sums -> row j (lanes 16j..16j+15) holds the 64-lane sum of a_j.
-__device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3) {
-    swap32(a0, a2);
-    float r = a0 + a2;
-    swap32(a1, a3);
-    float q = a1 + a3;
-    swap16(r, q);
-    float v = r + q;
-    v += dpp_row<0xB1>(v);    // quad_perm [1,0,3,2]
-    v += dpp_row<0x4E>(v);    // quad_perm [2,3,0,1]
-    v += dpp_row<0x141>(v);   // row_half_mirror
-    v += dpp_row<0x140>(v);   // row_mirror
-    return v;
-}
-
 template <int NE>
 __device__ __forceinline__ void load_row(float (&r)[NE], const float *__restrict__ p, int lane, int dim) {
 #pragma unroll
@@ -175,14 +139,6 @@ __device__ __forceinline__ void store_row(float *p, const float (&r)[NE], int la
 #pragma unroll
     for (int i = 0; i < NE; ++i)
         if (lane + i * kWave < dim) p[lane + i * kWave] = r[i];
-}
-
-template <int NE>
-__device__ __forceinline__ float dot_partial(const float (&x)[NE], const float (&y)[NE]) {
-    float s = 0.0f;
-#pragma unroll
-    for (int i = 0; i < NE; ++i) s = fmaf(x[i], y[i], s);
-    return s;
 }
 
 // Partial dot product with target slot t, zero for the padding slots of the last group of four.

@@ -285,23 +285,32 @@ struct LLArgs {
     const int32_t *kept_vid;
     const uint32_t *kept_meta;
     const int32_t *doc_kept;
-    int64_t n_docs;
+    int64_t n_units;        // work units: kSegLen consecutive kept centres of one document
+    int32_t segs_per_doc;
     int32_t doc_len;
-    double *doc_ll;
-    int64_t *doc_nodes;
+    double *unit_ll;
+    int64_t *unit_nodes;
 };
 
-template <int NE>
+// One wavefront per work unit (a fixed assignment, so the sums are the same from run to run).
+// Per centre the path is walked once for a group of up to G window words: four node rows at a
+// time (the next four loaded while the current ones are used), the G x 4 dot products reduced
+// four at a time; lane n collects the dot products of path node n, and takes the log-sigmoids
+// of its node for every pair of the group in fp64.
+template <int NE, int G>
 __global__ __launch_bounds__(256) void k_loglik(LLArgs a) {
     const int lane = lane_id();
     const int64_t wave0 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
     const int64_t nwaves = static_cast<int64_t>(gridDim.x) * blockDim.x / kWave;
-    for (int64_t d = wave0; d < a.n_docs; d += nwaves) {
+    for (int64_t u = wave0; u < a.n_units; u += nwaves) {
+        const int64_t d = u / a.segs_per_doc;
         const int nk = a.doc_kept[d];
+        const int j0 = static_cast<int>(u - d * a.segs_per_doc) * kSegLen;
+        const int j1 = min(nk, j0 + kSegLen);
         const int64_t base = d * a.doc_len;
         double acc = 0.0;
         int64_t nodes = 0;
-        for (int j = 0; j < nk; ++j) {
+        for (int j = j0; j < j1; ++j) {
             const int v = a.kept_vid[base + j];
             const int eff = static_cast<int>(a.kept_meta[base + j] >> 16);
             const int clo = max(0, j - eff), chi = min(nk - 1, j + eff);
@@ -309,44 +318,68 @@ __global__ __launch_bounds__(256) void k_loglik(LLArgs a) {
             const int len = a.codelen[v];
             const uint64_t code = a.code[v];
             const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
-            for (int p = 0; p < P; ++p) {
-                const int c = clo + p + ((clo + p >= j) ? 1 : 0);
-                const int w = a.kept_vid[base + c];
-                float x[NE];
+            // lane q: the q-th window word (centre excluded)
+            const int cq = clo + lane + ((clo + lane >= j) ? 1 : 0);
+            const int my_w = (lane < P) ? a.kept_vid[base + cq] : 0;
+            const double sign = ((code >> min(lane, 63)) & 1ull) ? -1.0 : 1.0;
+            for (int g0 = 0; g0 < P; g0 += G) {
+                const int nx = min(G, P - g0);
+                float x[G][NE], mine[G];
 #pragma unroll
-                for (int i = 0; i < NE; ++i) {
-                    const int col = lane + i * kWave;
-                    x[i] = col < a.dim ? a.syn0[static_cast<int64_t>(w) * a.stride + col] : 0.0f;
+                for (int p = 0; p < G; ++p) {
+                    const int w = __builtin_amdgcn_readlane(my_w, min(g0 + p, kWave - 1));
+                    buf_load_row<NE>(x[p], row_rsrc(const_cast<float *>(a.syn0), p < nx ? w : 0, a.stride,
+                                                    p < nx ? a.dim * 4 : 0), lane);
+                    mine[p] = 0.0f;
                 }
-                float mine = 0.0f;   // lane jn keeps the dot product of node jn
-                for (int jn = 0; jn < len; ++jn) {
-                    const int n = __builtin_amdgcn_readlane(my_pt, jn);
-                    float s = 0.0f;
+                float y[4][NE], yn[4][NE];
 #pragma unroll
-                    for (int i = 0; i < NE; ++i) {
-                        const int col = lane + i * kWave;
-                        const float y = col < a.dim ? a.syn1[static_cast<int64_t>(n) * a.stride + col] : 0.0f;
-                        s = fmaf(x[i], y, s);
+                for (int r = 0; r < 4; ++r) {
+                    const int n = __builtin_amdgcn_readlane(my_pt, min(r, kWave - 1));
+                    buf_load_row<NE>(y[r], row_rsrc(const_cast<float *>(a.syn1), r < len ? n : 0, a.stride,
+                                                    r < len ? a.dim * 4 : 0), lane);
+                }
+                for (int c0 = 0; c0 < len; c0 += 4) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int c = c0 + 4 + r;
+                        const int n = __builtin_amdgcn_readlane(my_pt, min(c, kWave - 1));
+                        buf_load_row<NE>(yn[r], row_rsrc(const_cast<float *>(a.syn1), c < len ? n : 0, a.stride,
+                                                         c < len ? a.dim * 4 : 0), lane);
                     }
-                    const float z = wave_sum(s);
-                    if (lane == jn) mine = z;
+#pragma unroll
+                    for (int p = 0; p < G; ++p) {
+                        if (p < nx) {
+                            const float z = reduce4(dot_partial<NE>(x[p], y[0]), dot_partial<NE>(x[p], y[1]),
+                                                    dot_partial<NE>(x[p], y[2]), dot_partial<NE>(x[p], y[3]));
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                const float zr = __builtin_bit_cast(
+                                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, z), 16 * r));
+                                mine[p] = (lane == c0 + r) ? zr : mine[p];
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+#pragma unroll
+                        for (int i = 0; i < NE; ++i) y[r][i] = yn[r][i];
                 }
-                if (lane < len) {
-                    const double sign = ((code >> lane) & 1ull) ? -1.0 : 1.0;
-                    acc += log_sigmoid(sign * static_cast<double>(mine));
-                }
-                nodes += len;
+#pragma unroll
+                for (int p = 0; p < G; ++p)
+                    if (p < nx && lane < len) acc += log_sigmoid(sign * static_cast<double>(mine[p]));
             }
+            nodes += static_cast<int64_t>(P) * len;
         }
         acc = wave_sum(acc);
         if (lane == 0) {
-            a.doc_ll[d] = acc;
-            a.doc_nodes[d] = nodes;
+            a.unit_ll[u] = acc;
+            a.unit_nodes[u] = nodes;
         }
     }
 }
 
-// fixed-order sum of per-document partials
+// fixed-order sum of the work units' partials
 __global__ __launch_bounds__(1024) void k_sum_docs(const double *__restrict__ ll, const int64_t *__restrict__ nodes,
                                                    int64_t n, double *__restrict__ out_ll,
                                                    int64_t *__restrict__ out_nodes) {
@@ -375,22 +408,27 @@ __global__ __launch_bounds__(1024) void k_sum_docs(const double *__restrict__ ll
 }
 
 using LLFn = void (*)(LLArgs);
+// G window words per path walk: all of a window of half-width 5 for rows of up to 320 floats.
 LLFn pick_ll(int dim) {
     const int ne = (dim + kWave - 1) / kWave;
-    if (ne <= 1) return k_loglik<1>;
-    if (ne <= 2) return k_loglik<2>;
-    if (ne <= 4) return k_loglik<4>;
-    if (ne <= 5) return k_loglik<5>;
-    if (ne <= 8) return k_loglik<8>;
-    return k_loglik<16>;
+    if (ne <= 1) return k_loglik<1, 10>;
+    if (ne <= 2) return k_loglik<2, 10>;
+    if (ne <= 4) return k_loglik<4, 10>;
+    if (ne <= 5) return k_loglik<5, 10>;
+    if (ne <= 8) return k_loglik<8, 4>;
+    return k_loglik<16, 2>;
 }
 
 }  // namespace
 
-size_t loglik_extra_bytes(int64_t n_docs) {
+int64_t loglik_units(int64_t n_tokens, int32_t doc_len) {
+    return std::max<int64_t>(1, ceil_div(n_tokens, doc_len)) * segs_per_doc(doc_len);
+}
+
+size_t loglik_extra_bytes(int64_t n_units) {
     Carve c;
-    c.take<double>(static_cast<size_t>(n_docs));
-    c.take<int64_t>(static_cast<size_t>(n_docs));
+    c.take<double>(static_cast<size_t>(n_units));
+    c.take<int64_t>(static_cast<size_t>(n_units));
     c.take<double>(1);
     c.take<int64_t>(1);
     return c.used();
@@ -398,7 +436,7 @@ size_t loglik_extra_bytes(int64_t n_docs) {
 
 int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
                double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, hipStream_t s) {
-    const int64_t n_docs = std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len));
+    const int64_t n_units = loglik_units(n_tokens, p->doc_len);
     LLArgs a{};
     a.syn0 = m->syn0;
     a.syn1 = m->syn1;
@@ -411,24 +449,25 @@ int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int
     a.kept_vid = b.kept_vid;
     a.kept_meta = b.kept_meta;
     a.doc_kept = b.doc_kept;
-    a.n_docs = n_tokens > 0 ? ceil_div(n_tokens, p->doc_len) : 0;
+    a.segs_per_doc = segs_per_doc(p->doc_len);
+    a.n_units = n_tokens > 0 ? ceil_div(n_tokens, p->doc_len) * a.segs_per_doc : 0;
     a.doc_len = p->doc_len;
-    a.doc_ll = c.take<double>(static_cast<size_t>(n_docs));
-    a.doc_nodes = c.take<int64_t>(static_cast<size_t>(n_docs));
+    a.unit_ll = c.take<double>(static_cast<size_t>(n_units));
+    a.unit_nodes = c.take<int64_t>(static_cast<size_t>(n_units));
     double *out = c.take<double>(1);
     int64_t *out_nodes = c.take<int64_t>(1);
-    if (a.n_docs > 0) {
+    if (a.n_units > 0) {
         const unsigned grid =
-            static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_docs, 4), 16LL * device_cu_count()));
+            static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_units, 4), 16LL * device_cu_count()));
         hipLaunchKernelGGL(pick_ll(m->dim), dim3(grid), dim3(256), 0, s, a);
         W2V_LAUNCH_CHECK("k_loglik");
-        k_sum_docs<<<1, 1024, 0, s>>>(a.doc_ll, a.doc_nodes, a.n_docs, out, out_nodes);
+        k_sum_docs<<<1, 1024, 0, s>>>(a.unit_ll, a.unit_nodes, a.n_units, out, out_nodes);
         W2V_LAUNCH_CHECK("k_sum_docs");
     }
     double hll = 0.0;
     int64_t nn = 0;
     int64_t tot[4] = {0, 0, 0, 0};
-    if (a.n_docs > 0) {
+    if (a.n_units > 0) {
         W2V_HIP(hipMemcpyAsync(&hll, out, sizeof(hll), hipMemcpyDeviceToHost, s));
         W2V_HIP(hipMemcpyAsync(&nn, out_nodes, sizeof(nn), hipMemcpyDeviceToHost, s));
     }

@@ -45,46 +45,6 @@ __device__ __forceinline__ float sigmoid_fast(float z) { return __builtin_amdgcn
 
 __device__ __forceinline__ void lds_add(float *p, float v) { atomicAdd(p, v); }
 
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
-}
-
-// Sum over the 16 lanes of each row, result in every lane of the row.
-__device__ __forceinline__ float row_sum(float v) {
-    v += dpp<0xB1>(v);    // quad_perm [1,0,3,2]
-    v += dpp<0x4E>(v);    // quad_perm [2,3,0,1]
-    v += dpp<0x141>(v);   // row_half_mirror
-    v += dpp<0x140>(v);   // row_mirror
-    return v;
-}
-
-// Swap the upper 32 lanes of a with the lower 32 lanes of b (permlane32), or the
-// odd rows of a with the even rows of b (permlane16).
-__device__ __forceinline__ void swap32(float &a, float &b) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
-                                                    false, false);
-    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
-    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
-}
-__device__ __forceinline__ void swap16(float &a, float &b) {
-    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, a), __builtin_bit_cast(unsigned, b),
-                                                    false, false);
-    a = __builtin_bit_cast(float, static_cast<unsigned>(r[0]));
-    b = __builtin_bit_cast(float, static_cast<unsigned>(r[1]));
-}
-
-// Four per-lane partial sums -> one register whose row j (lanes 16j..16j+15)
-// holds the full 64-lane sum of a_j.
-__device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3) {
-    swap32(a0, a2);
-    float r = a0 + a2;   // lanes 0-31: a0, lanes 32-63: a2 (each summed over lane pairs l, l+32)
-    swap32(a1, a3);
-    float q = a1 + a3;   // lanes 0-31: a1, lanes 32-63: a3
-    swap16(r, q);
-    return row_sum(r + q);   // rows: a0 a1 a2 a3
-}
-
 // One wave writes the cache's change back to HBM and re-bases val/orig on the
 // result. LDS rows are ls floats apart (ls >= dim, padding kept at zero). The
 // cache_k * dim elements go kFlushBatch per lane at a time: their atomic adds are
@@ -205,14 +165,6 @@ template <int NE>
 __device__ __forceinline__ void zero_row(float (&r)[NE]) {
 #pragma unroll
     for (int i = 0; i < NE; ++i) r[i] = 0.0f;
-}
-
-template <int NE>
-__device__ __forceinline__ float dot_partial(const float (&x)[NE], const float (&y)[NE]) {
-    float s = 0.0f;
-#pragma unroll
-    for (int i = 0; i < NE; ++i) s = fmaf(x[i], y[i], s);
-    return s;
 }
 
 // Rows of nodes c0 .. c0+3 of the path (zeros past its end), from LDS when cached.
