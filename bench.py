@@ -15,7 +15,13 @@ Byte model, per kept centre v with P > 0 window words (fp32 rows of d floats):
   + 8 d P                      window rows read once and updated once
   + 4 len(v) + 9               path indices, code, length
 plus the cache traffic of each workgroup: fill 4 d k, write-back 8 d k per
-flush and at the end.
+flush and at the end. When the word rows of a span of H kept positions on
+each side of the centre stay in registers across centres (write_policy bit 3),
+the 8 d P term becomes 8 d per row entering a span: per work unit (a segment of
+consecutive kept centres j0 .. j1-1 of a document with nk kept words) the
+rows of its first centre's span, then per later centre the previous centre's
+row and the row H positions ahead when it exists; each is read once and
+written back once.
 """
 from __future__ import annotations
 
@@ -44,7 +50,8 @@ def parse():
     ap.add_argument("--flush-policy", type=int, default=1)
     ap.add_argument("--cache-mode", type=int, default=0, help="0 = cached copy and original, 1 = delta-only")
     ap.add_argument("--write-policy", type=int, default=None,
-                    help="default 7 (every row stored); with --ns, 1 (target rows stored, word rows added)")
+                    help="default 15 (every row stored, word rows kept across centres); with --ns, 1 (target "
+                         "rows stored, word rows added)")
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
     ap.add_argument("--no-probe", action="store_true", help="skip the random-row memory probe")
@@ -60,7 +67,7 @@ def parse():
                     help="first write, then read, 1.28 GB of rows once each (reference dispatches for HBM byte counters)")
     args = ap.parse_args()
     if args.write_policy is None:
-        args.write_policy = 1 if args.ns else 7
+        args.write_policy = 1 if args.ns else 15
     return args
 
 
@@ -86,7 +93,23 @@ def algorithmic_bytes(torch, voc, tree, mask, doc_len, dim, k, flush_every, n_gr
     centres = int(v.numel())
     node_rows = int(unc[v].sum().item())
     path_len = int(lens[v].sum().item())
-    return centres, node_rows, path_len
+    return centres, node_rows, path_len, per_doc.where(per_doc >= 2, 0)
+
+
+def span_rows(torch, per_doc, span, seg_len=128):
+    """Word rows entering a span of `span` kept positions each side of the centre, over every work unit."""
+    nk = per_doc.to(torch.int64)
+    n_seg = (nk + seg_len - 1) // seg_len
+    doc = torch.repeat_interleave(torch.arange(nk.numel(), device=nk.device), n_seg)
+    first = torch.repeat_interleave(n_seg.cumsum(0) - n_seg, n_seg)
+    j0 = (torch.arange(doc.numel(), device=nk.device) - first) * seg_len
+    nkd = nk[doc]
+    j1 = torch.minimum(nkd, j0 + seg_len)
+    zero = torch.zeros_like(j0)
+    start = torch.clamp(j0, max=span) + torch.clamp(nkd - 1 - j0, max=span)
+    behind = j1 - 1 - j0                                                   # previous centre's row
+    ahead = torch.maximum(zero, torch.minimum(j1 - 2, nkd - 2 - span) - j0 + 1)   # row span positions ahead
+    return int((start + behind + ahead).sum().item())
 
 
 def main():
@@ -149,9 +172,12 @@ def main():
 
     # byte model of one launch (the sampler's keep mask with the training seed)
     pr = w2v.sample_pairs(voc.tokens, voc.V, voc.vocab_counts, voc.train_words, p, cap=0, want_mask=True)
-    centres, node_rows, path_len = algorithmic_bytes(torch, voc, tree, pr.keep_mask, p.doc_len, w.dim,
-                                                     args.cache_k, args.flush_every, 0)
+    centres, node_rows, path_len, per_doc = algorithmic_bytes(torch, voc, tree, pr.keep_mask, p.doc_len, w.dim,
+                                                              args.cache_k, args.flush_every, 0)
     pairs = pr.total
+    span = w2v.train_word_span(model, p)
+    word_rows = span_rows(torch, per_doc, span) if span else pairs
+    del per_doc
     del pr
     torch.cuda.empty_cache()
 
@@ -192,7 +218,7 @@ def main():
     d = w.dim
     n_groups, n_waves = w2v.last_train_launch()
     flushes = centres // max(1, args.flush_every) + n_groups
-    byte_total = (8 * d * node_rows + 8 * d * pairs + 4 * path_len + 9 * centres
+    byte_total = (8 * d * node_rows + 8 * d * word_rows + 4 * path_len + 9 * centres
                   + n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k)
     achieved = byte_total / (kernel_ms / 1e3) / 1e9
     res = w2v.last_train_resources()

@@ -139,7 +139,15 @@ typedef struct {
                                 overwritten, as in Hogwild) instead of atomically adding their change;
                                 bit 1: the same for the word vectors syn0 (a word repeated within a window
                                 stores at its first position and adds the change of the others);
-                                bit 2: the same for the cached rows in the workgroup's LDS copy */
+                                bit 2: the same for the cached rows in the workgroup's LDS copy;
+                                bit 3 (needs bit 1): skip-gram word rows kept across centres -- a wavefront
+                                holds the rows of the kept words within `window` positions of its centre in
+                                registers while it walks a document's centres in order, loading a row when it
+                                enters that span and storing it when it leaves or becomes the centre (one read
+                                and write per word and span instead of one per pair). Applies to rows of 129 to
+                                512 floats on the store-only walk (bit 0; bit 2 when cache_k > 0; hot_k 0;
+                                cache_mode 0) with window <= 5 (<= 2 above 320 floats); elsewhere the bit is
+                                ignored; w2v_train_word_span reports which */
     int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), 1 = add the
                                 change divided by the number of workgroups (their progress averaged) */
     int32_t hot_k;           /* with write_policy bit 0: the hot_k inner nodes created just before the cached
@@ -197,6 +205,14 @@ typedef struct {
 size_t w2v_train_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
 int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,
                        int64_t *stats, void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/* Half-width of the word-row span that w2v_train_hs_epoch keeps in registers
+   for these arguments (write_policy bit 3): the rows of the kept words within
+   that many positions of the centre stay in registers across centres; 0 when
+   every centre reads and writes its window rows itself. Host-side, no launch;
+   returns -1 for a NULL pointer or an invalid model or parameter block
+   (w2v_last_error says which). */
+int32_t w2v_train_word_span(const w2v_model *m, const w2v_params *p);
 
 /* Duration in milliseconds of the main training kernel of the last
    w2v_train_hs_epoch call on the calling thread's current device (HIP events

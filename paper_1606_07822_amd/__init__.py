@@ -79,6 +79,8 @@ def lib() -> ctypes.CDLL:
                                          ctypes.c_size_t, P]
         L.w2v_last_train_kernel_ms.restype = ctypes.c_int
         L.w2v_last_train_kernel_ms.argtypes = [ctypes.POINTER(ctypes.c_float)]
+        L.w2v_train_word_span.restype = I32
+        L.w2v_train_word_span.argtypes = [ctypes.POINTER(CModel), ctypes.POINTER(CParams)]
         L.w2v_last_train_launch.restype = ctypes.c_int
         L.w2v_last_train_launch.argtypes = [ctypes.POINTER(I32), ctypes.POINTER(I32)]
         L.w2v_hs_loglik_workspace_bytes.restype = ctypes.c_size_t
@@ -327,6 +329,17 @@ def train_workspace_bytes(model: Model, n_tokens: int, p: Params) -> int:
     if cp.corpus_tokens <= 0:
         cp.corpus_tokens = n_tokens
     return int(lib().w2v_train_workspace_bytes(ctypes.byref(cm), n_tokens, ctypes.byref(cp)))
+
+
+def train_word_span(model: Model, p: Params) -> int:
+    """Half-width of the word-row span kept in registers across centres for these settings (0: none)."""
+    cm, cp = model.c(), p.c()
+    if cp.corpus_tokens <= 0:
+        cp.corpus_tokens = 1
+    h = int(lib().w2v_train_word_span(ctypes.byref(cm), ctypes.byref(cp)))
+    if h < 0:
+        raise W2VError(W2V_E_ARG, last_error())
+    return h
 
 
 def last_train_kernel_ms() -> float:

@@ -21,8 +21,10 @@ int run_sample_pairs(const int32_t *, int64_t, int32_t, const int64_t *, int64_t
                      int64_t *, int64_t, uint8_t *, int64_t *, int64_t *, uint64_t *, void *, hipStream_t);
 size_t train_lds_bytes(int32_t cache_k, int32_t dim, bool delta);
 int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int workers, int64_t n_units, int *grid,
-                       int *waves);
+                       int *waves,
+                       bool slide = false);
 int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, int waves);
+int train_word_span(int arch, int dim, bool buf, int write_policy, int window);
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals);
 size_t sync_extra_bytes(int32_t V, int32_t dim, int64_t n_docs);
@@ -148,7 +150,9 @@ int check_params(const w2v_params *p, bool training) {
         if (p->flush_every < 1) return fail(W2V_E_ARG, "flush_every must be >= 1");
         if (p->mode == 1 && p->sync_batch < 1) return fail(W2V_E_ARG, "sync_batch must be >= 1");
         if (p->workers < 0) return fail(W2V_E_ARG, "workers must be >= 0");
-        if (p->write_policy < 0 || p->write_policy > 7) return fail(W2V_E_ARG, "write_policy must be in 0..7");
+        if (p->write_policy < 0 || p->write_policy > 15) return fail(W2V_E_ARG, "write_policy must be in 0..15");
+        if ((p->write_policy & 8) && !(p->write_policy & 2))
+            return fail(W2V_E_ARG, "write_policy bit 3 (word rows kept across centres) needs bit 1 (word rows stored)");
         if (p->flush_policy != 0 && p->flush_policy != 1) return fail(W2V_E_ARG, "flush_policy must be 0 or 1");
         if (p->cache_mode != 0 && p->cache_mode != 1) return fail(W2V_E_ARG, "cache_mode must be 0 or 1");
         if (p->hot_k < 0) return fail(W2V_E_ARG, "hot_k must be >= 0");
@@ -360,6 +364,18 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     if (int rc = timing_events(&ev0, &ev1)) return rc;
     return launch_train_async(a, p->arch, p->window, ev0, ev1, s, stats, b.totals);
+}
+
+int32_t w2v_train_word_span(const w2v_model *m, const w2v_params *p) {
+    g_err.clear();
+    if (!m || !p) {
+        fail(W2V_E_ARG, "a required pointer is NULL");
+        return -1;
+    }
+    if (check_model(m, false) != W2V_OK || check_params(p, true) != W2V_OK) return -1;
+    if (p->mode != 0) return 0;
+    const int32_t wp = kernel_write_policy(p);
+    return train_word_span(p->arch, m->dim, train_stores_only(wp, p->cache_k, p->hot_k, m->dim), wp, p->window);
 }
 
 int w2v_last_train_kernel_ms(float *ms_host) {

@@ -47,11 +47,14 @@ __device__ __forceinline__ void lds_add(float *p, float v) { atomicAdd(p, v); }
 
 // One wave writes the cache's change back to HBM and re-bases val/orig on the
 // result. LDS rows are ls floats apart (ls >= dim, padding kept at zero). The
-// cache_k * dim elements go kFlushBatch per lane at a time: their atomic adds are
+// cache_k * dim elements go B per lane at a time: their atomic adds are
 // all issued before the first returned value is used, so a flush costs a few
-// round trips to memory rather than one per row and column.
+// round trips to memory rather than one per row and column. (B = 16; a kernel
+// that keeps word rows in registers across centres uses fewer, as those rows
+// stay live through the flush.)
 constexpr int kFlushBatch = 16;
 
+template <int B>
 __device__ void flush_cache_wave(const TrainArgs &a, bool delta, float *val, float *orig, int ls, int lane) {
     const int n = a.cache_k * a.dim;
     if (delta) {
@@ -67,11 +70,11 @@ __device__ void flush_cache_wave(const TrainArgs &a, bool delta, float *val, flo
         }
         return;
     }
-    for (int i0 = 0; i0 < n; i0 += kFlushBatch * kWave) {
-        float c[kFlushBatch], d[kFlushBatch], old[kFlushBatch];
-        int li[kFlushBatch];
+    for (int i0 = 0; i0 < n; i0 += B * kWave) {
+        float c[B], d[B], old[B];
+        int li[B];
 #pragma unroll
-        for (int b = 0; b < kFlushBatch; ++b) {
+        for (int b = 0; b < B; ++b) {
             const int i = i0 + b * kWave + lane;
             const int s = i / a.dim, col = i - s * a.dim;
             li[b] = s * ls + col;
@@ -85,7 +88,7 @@ __device__ void flush_cache_wave(const TrainArgs &a, bool delta, float *val, flo
             }
         }
 #pragma unroll
-        for (int b = 0; b < kFlushBatch; ++b) {
+        for (int b = 0; b < B; ++b) {
             if (d[b] != 0.0f) {
                 const float nv = old[b] + d[b];
                 lds_add(val + li[b], nv - c[b]);
@@ -239,17 +242,18 @@ __device__ __forceinline__ void fetch_centre(const TrainArgs &a, int4 r, const i
     }
 }
 
-// Every input x[0..nx), in order, updates the nc live rows of the chunk held in
+// Every input x[p0..p1), in order, updates the nc live rows of the chunk held in
 // yc (dot, sigmoid, gradient, then e += g y and y += g x for each row).
 template <int NE, int PG>
 __device__ __forceinline__ void chunk_update(float (&yc)[kChunk][NE], const float (&x)[PG][NE], float (&e)[PG][NE],
-                                             int nx, int nc, int c0, uint64_t code, float alpha, int lane) {
+                                             int p0, int p1, int nc, int c0, uint64_t code, float alpha,
+                                             int lane) {
     const int bitpos = c0 + (lane >> 4);
     const float t = (bitpos < 64) ? static_cast<float>((code >> bitpos) & 1ull) : 0.0f;
     const float one_minus_t = 1.0f - t;
 #pragma unroll
     for (int p = 0; p < PG; ++p) {
-        if (p < nx) {
+        if (p >= p0 && p < p1) {
             const float z = reduce4(dot_partial<NE>(x[p], yc[0]), dot_partial<NE>(x[p], yc[1]),
                                     dot_partial<NE>(x[p], yc[2]), dot_partial<NE>(x[p], yc[3]));
             const float gr = (one_minus_t - sigmoid_fast(z)) * alpha;
@@ -316,11 +320,11 @@ __device__ __forceinline__ void chunk_write_delta(const TrainArgs &a, float *val
 [[maybe_unused]] constexpr int kPfNone = 0;
 constexpr int kPfAll = 1, kPfSuffix = 2, kPfBuf = 3;
 
-// Walk the path of the centre with the inputs x[0..nx) (in order), accumulating
-// the hidden-layer gradients into e[0..nx). PG = compile-time bound of nx.
+// Walk the path of the centre with the inputs x[p0..p1) (in order), accumulating
+// the hidden-layer gradients into e[p0..p1). PG = size of the input arrays.
 template <int NE, int PG, int PF>
 __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const float (&x)[PG][NE],
-                                          float (&e)[PG][NE], int nx, int my_pt, int len, uint64_t code, float alpha,
+                                          float (&e)[PG][NE], int p0, int p1, int my_pt, int len, uint64_t code, float alpha,
                                           int lane) {
     float yc[kChunk][NE], y0[kChunk][NE];
     if constexpr (PF == kPfBuf) {
@@ -348,7 +352,7 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
                 }
             }
             const int nc = min(kChunk, len - c0);
-            chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+            chunk_update<NE, PG>(yc, x, e, p0, p1, nc, c0, code, alpha, lane);
 #pragma unroll
             for (int j = 0; j < kChunk; ++j) {
                 const int n = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
@@ -375,7 +379,7 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
 #pragma unroll
                 for (int i = 0; i < NE; ++i) y0[j][i] = yc[j][i];
             const int nc = min(kChunk, len - c0);
-            chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+            chunk_update<NE, PG>(yc, x, e, p0, p1, nc, c0, code, alpha, lane);
             chunk_write_delta<NE>(a, val, yc, y0, my_pt, c0, nc, lane);
             if (c0 + kChunk < len) {
 #pragma unroll
@@ -403,7 +407,7 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
 #pragma unroll
             for (int i = 0; i < NE; ++i) y0[j][i] = yc[j][i];
         const int nc = min(kChunk, len - c0);
-        chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+        chunk_update<NE, PG>(yc, x, e, p0, p1, nc, c0, code, alpha, lane);
         chunk_write_delta<NE>(a, val, yc, y0, my_pt, c0, nc, lane);
     }
     if constexpr (PF == kPfSuffix) {
@@ -412,7 +416,7 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
         for (; c0 < len; c0 += kChunk) {
             if (c0 + kChunk < len) load_chunk<NE>(y0, a, val, my_pt, c0 + kChunk, len, lane);
             const int nc = min(kChunk, len - c0);
-            chunk_update<NE, PG>(yc, x, e, nx, nc, c0, code, alpha, lane);
+            chunk_update<NE, PG>(yc, x, e, p0, p1, nc, c0, code, alpha, lane);
 #pragma unroll
             for (int j = 0; j < kChunk; ++j) {
                 if (j < nc) {
@@ -433,10 +437,129 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
     }
 }
 
+// Word rows kept across centres (write_policy bit 3, skip-gram): while a wavefront walks the
+// centres of a segment in order, the rows of the words at kept positions j-H .. j-1 and
+// j+1 .. j+H of the current centre j (H = PG/2) stay in registers. Slot q < H holds position
+// j-H+q, slot q >= H position j+1+q-H, so a centre's window words are the contiguous slots
+// H-(j-lo) .. H+(hi-j)-1, in window order. A row is loaded when its position comes within H of
+// the centre and stored when it leaves the span or becomes the centre, so each word row is read
+// and written about twice per centre instead of once per pair. Slots holding the same word are
+// kept equal: a change made to one is added to the others, and a word entering the span is copied
+// from a slot that holds it rather than read from memory.
+template <int PG>
+__device__ __forceinline__ bool span_has_dup(int sid, int lane) {
+    uint64_t any = 0;
+#pragma unroll
+    for (int q = 0; q < PG - 1; ++q) {
+        const int w = __builtin_amdgcn_readlane(sid, q);
+        any |= __ballot(w >= 0 && lane > q && lane < PG && sid == w);
+    }
+    return any != 0;
+}
+
+// Row of slot q from memory (zeros when the slot lies outside the document).
+template <int NE, int PG>
+__device__ __forceinline__ void span_load(float (&xw)[PG][NE], int q, const TrainArgs &a, int sid, int lane) {
+    const int w = __builtin_amdgcn_readlane(sid, q);
+    buf_load_row<NE>(xw[q], row_rsrc(a.syn0, w >= 0 ? w : 0, a.stride, w >= 0 ? a.dim * 4 : 0), lane);
+}
+
+template <int NE, int PG>
+__device__ __forceinline__ void span_store(const float (&xw)[PG][NE], int q, const TrainArgs &a, int sid, int lane) {
+    const int w = __builtin_amdgcn_readlane(sid, q);
+    store_row<NE>(a.syn0 + static_cast<int64_t>(w) * a.stride, xw[q], lane, a.dim, a.full_rows);
+}
+
+// Slot DST takes a new word w (sid already updated): a copy of a slot below PG - 1 other than DST
+// that holds w, else the row from memory. Returns the slot's dirty bit.
+template <int NE, int PG, int DST>
+__device__ __forceinline__ uint32_t span_enter(float (&xw)[PG][NE], const TrainArgs &a, int sid, uint32_t dirty,
+                                               int lane) {
+    const int w = __builtin_amdgcn_readlane(sid, DST);
+    const uint64_t m = w >= 0 ? __ballot(lane < PG - 1 && lane != DST && sid == w) : 0ull;
+    if (m == 0ull) {
+        span_load<NE, PG>(xw, DST, a, sid, lane);
+        return 0u;
+    }
+    // the copy goes through an empty asm statement per slot, which keeps the slots' branches apart (merged,
+    // they would become an indexed read of xw and move the whole array to scratch memory)
+    const uint64_t first = m & (~m + 1ull);
+#pragma unroll
+    for (int q = 0; q < PG - 1; ++q) {
+        if (first == (1ull << q)) {
+#pragma unroll
+            for (int i = 0; i < NE; ++i) {
+                float t = xw[q][i];
+                asm volatile("" : "+v"(t));
+                xw[DST][i] = t;
+            }
+        }
+    }
+    return (dirty >> __builtin_ctzll(m)) & 1u;
+}
+
+// After a centre: the active slots take their changes, which also go to every other slot of the same word.
+template <int NE, int PG>
+__device__ __forceinline__ void span_apply(float (&xw)[PG][NE], const float (&e)[PG][NE], int p0, int p1, int sid,
+                                           bool dup, uint32_t &dirty, int lane) {
+#pragma unroll
+    for (int q = 0; q < PG; ++q)
+        if (q >= p0 && q < p1)
+#pragma unroll
+            for (int i = 0; i < NE; ++i) xw[q][i] += e[q][i];
+    dirty |= ((1u << p1) - 1u) & ~((1u << p0) - 1u);
+    if (!dup) return;
+#pragma unroll
+    for (int q = 0; q < PG; ++q) {
+        if (q >= p0 && q < p1) {
+            const int w = __builtin_amdgcn_readlane(sid, q);
+            const uint64_t m = __ballot(lane < PG && lane != q && sid == w);
+#pragma unroll
+            for (int r = 0; r < PG; ++r) {
+                if ((m >> r) & 1ull) {
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) xw[r][i] += e[q][i];
+                    dirty |= 1u << r;
+                }
+            }
+        }
+    }
+}
+
+// Move the span from centre j to centre j+1: slot 0 (position j-H) and slot H (position j+1, the
+// next centre) leave, stored if changed; the rest shift down one slot; slot H-1 takes the old centre
+// word v and slot PG-1 the word at position j+1+H (w_edge, -1 past the document's end).
+template <int NE, int PG>
+__device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs &a, int &sid, uint32_t &dirty,
+                                           bool &dup, int v, int w_edge, int lane) {
+    constexpr int H = PG / 2;
+    constexpr uint32_t low = (1u << (H - 1)) - 1u;
+    if (dirty & 1u) span_store<NE, PG>(xw, 0, a, sid, lane);
+    if ((dirty >> H) & 1u) span_store<NE, PG>(xw, H, a, sid, lane);
+#pragma unroll
+    for (int q = 0; q + 1 < H; ++q)
+#pragma unroll
+        for (int i = 0; i < NE; ++i) xw[q][i] = xw[q + 1][i];
+#pragma unroll
+    for (int q = H; q + 1 < PG; ++q)
+#pragma unroll
+        for (int i = 0; i < NE; ++i) xw[q][i] = xw[q + 1][i];
+    dirty = ((dirty >> 1) & low) | (((dirty >> (H + 1)) & low) << H);
+    const int src = (lane < H - 1 || (lane >= H && lane < PG - 1)) ? lane + 1 : lane;
+    sid = __shfl(sid, src, kWave);
+    sid = lane == H - 1 ? v : (lane == PG - 1 ? w_edge : sid);
+    dirty |= span_enter<NE, PG, H - 1>(xw, a, sid, dirty, lane) << (H - 1);
+    dirty |= span_enter<NE, PG, PG - 1>(xw, a, sid, dirty, lane) << (PG - 1);
+    dup = span_has_dup<PG>(sid, lane);
+}
+
+
 // ARCH 0: skip-gram, window words in groups of PG; ARCH 1: CBOW (one input, the mean); ARCH 2: skip-gram
 // with the reversed orientation (the window word's path, the centre's vector as input).
-template <int NE, int PG, int ARCH, int WPB, int PF>
+// SLIDE (skip-gram, windows of at most PG/2 each side): word rows kept across centres.
+template <int NE, int PG, int ARCH, int WPB, int PF, bool SLIDE = false>
 __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
+    static_assert(!SLIDE || (ARCH == 0 && PF == kPfBuf && PG % 2 == 0), "word rows kept across centres: skip-gram");
     const int LS = lds_stride<NE>(a.dim);
     extern __shared__ float lds[];
     float *val = lds;
@@ -497,6 +620,18 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
             int wv_next = 0, pt_next = 0;
             fetch_centre<ARCH != 2>(a, centre_record<kRec>(a, rec, kv, km, j0, 0), kv, nk, j0, 0, lane, wv_next,
                                     pt_next);
+            constexpr int H = PG / 2;
+            float xw[SLIDE ? PG : 1][NE];
+            int sid = -1;
+            uint32_t dirty = 0;
+            bool dup = false;
+            if constexpr (SLIDE) {
+                const int pos = lane < H ? j0 - H + lane : j0 + 1 + lane - H;
+                sid = (lane < PG && pos >= 0 && pos < nk) ? kv[pos] : -1;
+#pragma unroll
+                for (int q = 0; q < PG; ++q) span_load<NE, PG>(xw, q, a, sid, lane);
+                dup = span_has_dup<PG>(sid, lane);
+            }
             for (int j = j0; j < j1; ++j) {
                 const int4 r = centre_record<kRec>(a, rec, kv, km, j0, j - j0);
                 const int v = __builtin_amdgcn_readfirstlane(r.x);
@@ -511,6 +646,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                 const int eff = static_cast<int>(meta >> 16);
                 const int lo = max(0, j - eff), hi = min(nk - 1, j + eff);
                 const int P = hi - lo;   // window words, centre excluded
+                [[maybe_unused]] const int w_edge = (SLIDE && j + 1 + H < nk) ? kv[j + 1 + H] : -1;
                 ++n_kept;
                 if (P > 0) {
                     const int64_t g = a.epoch_base + a.first_raw + base + static_cast<int64_t>(meta & 0xFFFFu);
@@ -518,7 +654,15 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     const int len = ARCH == 2 ? 0 : __builtin_amdgcn_readfirstlane(r.w);
                     const uint64_t code = ARCH == 2 ? 0 : a.code[v];
 
-                    if constexpr (ARCH == 0) {
+                    if constexpr (SLIDE) {
+                        const int p0 = H - (j - lo), p1 = H + (hi - j);
+                        float e[PG][NE];
+#pragma unroll
+                        for (int q = 0; q < PG; ++q) zero_row<NE>(e[q]);
+                        walk_path<NE, PG, PF>(a, val, xw, e, p0, p1, my_pt, len, code, alpha, lane);
+                        span_apply<NE, PG>(xw, e, p0, p1, sid, dup, dirty, lane);
+                        n_nodes += static_cast<uint64_t>(P) * len;
+                    } else if constexpr (ARCH == 0) {
                         // groups of PG window words walk the path in turn (one group when P <= PG). With
                         // several groups the hidden-layer gradients are parked in the wavefront's egrad
                         // rows and added to syn0 after the last group, so that every group reads the
@@ -541,7 +685,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                                 }
                                 zero_row<NE>(e[p]);
                             }
-                            walk_path<NE, PG, PF>(a, val, x, e, nx, my_pt, len, code, alpha, lane);
+                            walk_path<NE, PG, PF>(a, val, x, e, 0, nx, my_pt, len, code, alpha, lane);
                             if (defer) {
 #pragma unroll
                                 for (int p = 0; p < PG; ++p)
@@ -602,7 +746,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                             const uint64_t cw = a.code[w];
                             const int pw = (lane < lw) ? a.points[a.point_off[w] + lane] : 0;
                             zero_row<NE>(e[0]);
-                            walk_path<NE, 1, PF>(a, val, x, e, 1, pw, lw, cw, alpha, lane);
+                            walk_path<NE, 1, PF>(a, val, x, e, 0, 1, pw, lw, cw, alpha, lane);
 #pragma unroll
                             for (int i = 0; i < NE; ++i) x[0][i] += e[0][i];
                             nodes += lw;
@@ -630,7 +774,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                         const float fP = static_cast<float>(P);
 #pragma unroll
                         for (int i = 0; i < NE; ++i) h[0][i] = h[0][i] / fP;
-                        walk_path<NE, 1, PF>(a, val, h, e, 1, my_pt, len, code, alpha, lane);
+                        walk_path<NE, 1, PF>(a, val, h, e, 0, 1, my_pt, len, code, alpha, lane);
                         for (int p = 0; p < P; ++p) {
                             const int w = __builtin_amdgcn_readlane(wv, p);
                             float *xr = a.syn0 + static_cast<int64_t>(w) * a.stride;
@@ -656,11 +800,19 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     }
                     go = __builtin_amdgcn_readfirstlane(go);
                     if (go) {
-                        flush_cache_wave(a, delta, val, orig, LS, lane);
+                        flush_cache_wave<SLIDE ? 2 : kFlushBatch>(a, delta, val, orig, LS, lane);
                         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
                         if (lane == 0) atomicExch(&s_lock, 0);
                     }
                 }
+                if constexpr (SLIDE) {
+                    if (j + 1 < j1) span_shift<NE, PG>(xw, a, sid, dirty, dup, v, w_edge, lane);
+                }
+            }
+            if constexpr (SLIDE) {
+#pragma unroll
+                for (int q = 0; q < PG; ++q)
+                    if ((dirty >> q) & 1u) span_store<NE, PG>(xw, q, a, sid, lane);
             }
         }
     }
@@ -688,8 +840,10 @@ struct Variant {
 };
 
 template <int NE, int PG, int WPB, int PF>
-Variant variant(int arch) {
+Variant variant(int arch, bool slide) {
     constexpr int rb = rec_slots<NE>() ? WPB * kSegLen * static_cast<int>(sizeof(int4)) : 0;
+    if constexpr (PF == kPfBuf && NE >= 4 && PG % 2 == 0)
+        if (arch == 0 && slide) return Variant{k_train<NE, PG, 0, WPB, PF, true>, WPB, NE, PG, lds_stride<NE>, rb};
     if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE, PG, lds_stride<NE>, rb};
     if (arch == 2) return Variant{k_train<NE, 1, 2, WPB, PF>, WPB, NE, 1, lds_stride<NE>, rb};
     return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE, 1, lds_stride<NE>, rb};
@@ -699,14 +853,15 @@ Variant variant(int arch) {
 // prefetch) * 4 * NE. Occupancy beats prefetch: at dim 300, 3 waves per SIMD
 // without the prefetch ran 21 % faster than 2 with it.
 // buf: every row is written back by a store (train_stores_only), the pipelined walk.
-Variant pick_variant(int arch, int dim, bool buf) {
+// slide: skip-gram word rows kept across centres (the pipelined walk only; the caller checks the window).
+Variant pick_variant(int arch, int dim, bool buf, bool slide = false) {
     const int ne = (dim + kWave - 1) / kWave;
-    if (ne <= 1) return buf ? variant<1, 20, 16, kPfBuf>(arch) : variant<1, 20, 16, kPfAll>(arch);
-    if (ne <= 2) return buf ? variant<2, 20, 12, kPfBuf>(arch) : variant<2, 20, 12, kPfAll>(arch);
-    if (ne <= 4) return buf ? variant<4, 10, 12, kPfBuf>(arch) : variant<4, 10, 12, kPfAll>(arch);
-    if (ne <= 5) return buf ? variant<5, 10, 12, kPfBuf>(arch) : variant<5, 10, 12, kPfSuffix>(arch);
-    if (ne <= 8) return buf ? variant<8, 4, 8, kPfBuf>(arch) : variant<8, 4, 8, kPfSuffix>(arch);
-    return variant<16, 2, 8, kPfSuffix>(arch);
+    if (ne <= 1) return buf ? variant<1, 20, 16, kPfBuf>(arch, false) : variant<1, 20, 16, kPfAll>(arch, false);
+    if (ne <= 2) return buf ? variant<2, 20, 12, kPfBuf>(arch, false) : variant<2, 20, 12, kPfAll>(arch, false);
+    if (ne <= 4) return buf ? variant<4, 10, 12, kPfBuf>(arch, slide) : variant<4, 10, 12, kPfAll>(arch, false);
+    if (ne <= 5) return buf ? variant<5, 10, 12, kPfBuf>(arch, slide) : variant<5, 10, 12, kPfSuffix>(arch, false);
+    if (ne <= 8) return buf ? variant<8, 4, 8, kPfBuf>(arch, slide) : variant<8, 4, 8, kPfSuffix>(arch, false);
+    return variant<16, 2, 8, kPfSuffix>(arch, false);
 }
 
 __global__ void k_zero_train(int32_t *queue, unsigned long long *stats) {
@@ -732,8 +887,8 @@ size_t train_lds_bytes(int32_t cache_k, int32_t dim, bool delta) {
 }
 
 int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int workers, int64_t n_units, int *grid,
-                       int *waves) {
-    const Variant v = pick_variant(arch, dim, buf);
+                       int *waves, bool slide) {
+    const Variant v = pick_variant(arch, dim, buf, slide);
     if (workers > 0) {
         *grid = static_cast<int>(ceil_div(workers, v.waves_per_block));
         *waves = workers;
@@ -759,9 +914,22 @@ int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, 
     return static_cast<int64_t>(waves) * 2 * window * stride;
 }
 
+// Word rows kept across centres (write_policy bit 3 with bit 1): skip-gram on the pipelined walk, rows
+// of 129 to 512 floats (the narrower variants measured no faster with it), and a window whose both sides
+// fit the variant's register slots.
+bool train_slide(int arch, int dim, bool buf, int write_policy, int window) {
+    if (arch != 0 || !buf || (write_policy & 10) != 10 || dim <= 2 * kWave || dim > 8 * kWave) return false;
+    return 2 * window <= pick_variant(arch, dim, buf, true).pg;
+}
+
+int train_word_span(int arch, int dim, bool buf, int write_policy, int window) {
+    return train_slide(arch, dim, buf, write_policy, window) ? pick_variant(arch, dim, buf, true).pg / 2 : 0;
+}
+
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
                        int64_t *stats_out, const int64_t *totals) {
-    const Variant v = pick_variant(arch, a.dim, a.stores_only != 0);
+    const bool slide = train_slide(arch, a.dim, a.stores_only != 0, a.write_policy, window);
+    const Variant v = pick_variant(arch, a.dim, a.stores_only != 0, slide);
     const size_t lds = (a.cache_delta ? 1ull : 2ull) * a.cache_k * v.ls(a.dim) * sizeof(float);
     const int block = v.waves_per_block * kWave;
     a.full_rows = a.stride >= v.ne * kWave ? 1 : 0;
@@ -770,7 +938,7 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
                                     static_cast<int>(lds)));
     int grid = 0, waves = 0;
     if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.cache_delta != 0, a.stores_only != 0, a.workers,
-                                    a.n_units, &grid, &waves))
+                                    a.n_units, &grid, &waves, slide))
         return rc;
     a.workers = waves;
     if (train_egrad_floats(arch, a.dim, a.stores_only != 0, a.stride, window, waves) > 0) {

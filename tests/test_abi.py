@@ -115,7 +115,9 @@ def _params(w2v, **kw):
     ({}, dict(cache_k=100), "cache_k"),
     ({}, dict(alpha0=0.0), "alpha0"),
     ({}, dict(hot_k=-1), "hot_k"),
-    ({}, dict(write_policy=8), "write_policy"),
+    ({}, dict(write_policy=8), "needs bit 1"),
+    ({}, dict(write_policy=13), "needs bit 1"),
+    ({}, dict(write_policy=16), "write_policy"),
     ({}, dict(flush_policy=2), "flush_policy"),
     ({}, dict(cache_mode=2), "cache_mode"),
 ])
@@ -231,3 +233,38 @@ def test_launch_reports_need_pointers(w2v):
     a, b, c = ctypes.c_int32(-1), ctypes.c_int32(-1), ctypes.c_int32(-1)
     assert L.w2v_last_train_launch(None, ctypes.byref(b)) == w2v.W2V_E_ARG
     assert L.w2v_last_train_resources(ctypes.byref(a), None, ctypes.byref(c)) == w2v.W2V_E_ARG
+
+
+# Host-side choice of the skip-gram word-row span (write_policy bit 3): half-width or 0, no launch.
+@pytest.mark.parametrize("mk,pk,span", [
+    (dict(dim=300, row_stride=320), dict(write_policy=15, cache_k=31), 5),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, cache_k=0, window=3), 5),
+    (dict(dim=300, row_stride=320), dict(write_policy=11, cache_k=0), 5),
+    (dict(dim=150, row_stride=192), dict(write_policy=15, window=1), 5),
+    (dict(dim=129, row_stride=132), dict(write_policy=15), 5),
+    (dict(dim=128, row_stride=128), dict(write_policy=15), 0),
+    (dict(dim=50, row_stride=64), dict(write_policy=15), 0),
+    (dict(dim=450, row_stride=512), dict(write_policy=15, window=2), 2),
+    (dict(dim=450, row_stride=512), dict(write_policy=15, window=3), 0),
+    (dict(dim=600, row_stride=640), dict(write_policy=15, window=1), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, window=6), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=7), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=11, cache_k=31), 0),   # cached rows not stored
+    (dict(dim=300, row_stride=320), dict(write_policy=15, arch=1), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, arch=2), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, mode=1), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, hot_k=8), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, cache_mode=1), 0),
+])
+def test_train_word_span(w2v, mk, pk, span):
+    m = _model(w2v, **mk)
+    p = _params(w2v, **pk)
+    assert w2v.lib().w2v_train_word_span(ctypes.byref(m), ctypes.byref(p)) == span
+
+
+def test_train_word_span_argument_errors(w2v):
+    L = w2v.lib()
+    assert L.w2v_train_word_span(None, ctypes.byref(_params(w2v))) == -1
+    assert "NULL" in w2v.last_error()
+    assert L.w2v_train_word_span(ctypes.byref(_model(w2v)), ctypes.byref(_params(w2v, write_policy=8))) == -1
+    assert "needs bit 1" in w2v.last_error()

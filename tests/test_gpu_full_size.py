@@ -191,7 +191,7 @@ def test_full_single_worker_matches_oracle_centre_major(w2v, k, wp):
     np.testing.assert_array_equal(g1[:ov.V - 1][~touched1], syn1[~touched1])
 
 
-@pytest.mark.parametrize("wp", [5, 7])
+@pytest.mark.parametrize("wp", [5, 7, 15])
 def test_full_prefix_async_loglik_within_1pct(w2v, wp):
     g = golden(f"oracle_ll_{NAME}_first{PREFIX}.json")
     w, _, ov, _ = oracle_full()
