@@ -140,14 +140,15 @@ typedef struct {
                                 bit 1: the same for the word vectors syn0 (a word repeated within a window
                                 stores at its first position and adds the change of the others);
                                 bit 2: the same for the cached rows in the workgroup's LDS copy;
-                                bit 3 (needs bit 1): skip-gram word rows kept across centres -- a wavefront
+                                bit 3 (needs bit 1): word rows kept across centres -- a wavefront
                                 holds the rows of the kept words within `window` positions of its centre in
                                 registers while it walks a document's centres in order, loading a row when it
                                 enters that span and storing it when it leaves or becomes the centre (one read
                                 and write per word and span instead of one per pair). Applies to rows of 129 to
-                                512 floats on the store-only walk (bit 0; bit 2 when cache_k > 0; hot_k 0;
-                                cache_mode 0) with window <= 5 (<= 2 above 320 floats); elsewhere the bit is
-                                ignored; w2v_train_word_span reports which */
+                                512 floats with window <= 5: CBOW always, skip-gram on the store-only walk
+                                (bit 0; bit 2 when cache_k > 0; hot_k 0; cache_mode 0) and with window <= 2
+                                above 320 floats; elsewhere the bit is ignored; w2v_train_word_span reports
+                                which */
     int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), 1 = add the
                                 change divided by the number of workgroups (their progress averaged) */
     int32_t hot_k;           /* with write_policy bit 0: the hot_k inner nodes created just before the cached

@@ -526,6 +526,34 @@ __device__ __forceinline__ void span_apply(float (&xw)[PG][NE], const float (&e)
     }
 }
 
+// The same after a CBOW centre, where every active slot takes the one gradient e.
+template <int NE, int PG>
+__device__ __forceinline__ void span_apply_same(float (&xw)[PG][NE], const float (&e)[NE], int p0, int p1, int sid,
+                                                bool dup, uint32_t &dirty, int lane) {
+    // a slot's total: e once per active slot holding its word (itself included when active)
+    uint32_t mult[PG];
+#pragma unroll
+    for (int r = 0; r < PG; ++r) mult[r] = (r >= p0 && r < p1) ? 1u : 0u;
+    if (dup) {
+#pragma unroll
+        for (int q = 0; q < PG; ++q) {
+            if (q >= p0 && q < p1) {
+                const int w = __builtin_amdgcn_readlane(sid, q);
+                const uint64_t m = __ballot(lane < PG && lane != q && sid == w);
+#pragma unroll
+                for (int r = 0; r < PG; ++r) mult[r] += static_cast<uint32_t>((m >> r) & 1ull);
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < PG; ++r) {
+        for (uint32_t c = 0; c < mult[r]; ++c)
+#pragma unroll
+            for (int i = 0; i < NE; ++i) xw[r][i] += e[i];
+        if (mult[r]) dirty |= 1u << r;
+    }
+}
+
 // Move the span from centre j to centre j+1: slot 0 (position j-H) and slot H (position j+1, the
 // next centre) leave, stored if changed; the rest shift down one slot; slot H-1 takes the old centre
 // word v and slot PG-1 the word at position j+1+H (w_edge, -1 past the document's end).
@@ -559,7 +587,8 @@ __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs 
 // SLIDE (skip-gram, windows of at most PG/2 each side): word rows kept across centres.
 template <int NE, int PG, int ARCH, int WPB, int PF, bool SLIDE = false>
 __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
-    static_assert(!SLIDE || (ARCH == 0 && PF == kPfBuf && PG % 2 == 0), "word rows kept across centres: skip-gram");
+    static_assert(!SLIDE || (ARCH == 0 && PF == kPfBuf && PG % 2 == 0) || (ARCH == 1 && PG % 2 == 0),
+                  "word rows kept across centres: skip-gram on the store-only walk, or CBOW");
     const int LS = lds_stride<NE>(a.dim);
     extern __shared__ float lds[];
     float *val = lds;
@@ -654,7 +683,25 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     const int len = ARCH == 2 ? 0 : __builtin_amdgcn_readfirstlane(r.w);
                     const uint64_t code = ARCH == 2 ? 0 : a.code[v];
 
-                    if constexpr (SLIDE) {
+                    if constexpr (SLIDE && ARCH == 1) {
+                        // CBOW: h = mean of the active slots' rows (window order); one path walk; every
+                        // active slot takes the hidden-layer gradient
+                        const int p0 = H - (j - lo), p1 = H + (hi - j);
+                        float h[1][NE], e[1][NE];
+                        zero_row<NE>(h[0]);
+                        zero_row<NE>(e[0]);
+#pragma unroll
+                        for (int q = 0; q < PG; ++q)
+                            if (q >= p0 && q < p1)
+#pragma unroll
+                                for (int i = 0; i < NE; ++i) h[0][i] += xw[q][i];
+                        const float fP = static_cast<float>(P);
+#pragma unroll
+                        for (int i = 0; i < NE; ++i) h[0][i] = h[0][i] / fP;
+                        walk_path<NE, 1, PF>(a, val, h, e, 0, 1, my_pt, len, code, alpha, lane);
+                        span_apply_same<NE, PG>(xw, e[0], p0, p1, sid, dup, dirty, lane);
+                        n_nodes += len;
+                    } else if constexpr (SLIDE) {
                         const int p0 = H - (j - lo), p1 = H + (hi - j);
                         float e[PG][NE];
 #pragma unroll
@@ -844,6 +891,8 @@ Variant variant(int arch, bool slide) {
     constexpr int rb = rec_slots<NE>() ? WPB * kSegLen * static_cast<int>(sizeof(int4)) : 0;
     if constexpr (PF == kPfBuf && NE >= 4 && PG % 2 == 0)
         if (arch == 0 && slide) return Variant{k_train<NE, PG, 0, WPB, PF, true>, WPB, NE, PG, lds_stride<NE>, rb};
+    if constexpr (NE >= 4 && NE <= 8)   // CBOW keeps ten word slots (its walk has a single input row)
+        if (arch == 1 && slide) return Variant{k_train<NE, 10, 1, WPB, PF, true>, WPB, NE, 10, lds_stride<NE>, rb};
     if (arch == 0) return Variant{k_train<NE, PG, 0, WPB, PF>, WPB, NE, PG, lds_stride<NE>, rb};
     if (arch == 2) return Variant{k_train<NE, 1, 2, WPB, PF>, WPB, NE, 1, lds_stride<NE>, rb};
     return Variant{k_train<NE, 1, 1, WPB, PF>, WPB, NE, 1, lds_stride<NE>, rb};
@@ -858,9 +907,9 @@ Variant pick_variant(int arch, int dim, bool buf, bool slide = false) {
     const int ne = (dim + kWave - 1) / kWave;
     if (ne <= 1) return buf ? variant<1, 20, 16, kPfBuf>(arch, false) : variant<1, 20, 16, kPfAll>(arch, false);
     if (ne <= 2) return buf ? variant<2, 20, 12, kPfBuf>(arch, false) : variant<2, 20, 12, kPfAll>(arch, false);
-    if (ne <= 4) return buf ? variant<4, 10, 12, kPfBuf>(arch, slide) : variant<4, 10, 12, kPfAll>(arch, false);
-    if (ne <= 5) return buf ? variant<5, 10, 12, kPfBuf>(arch, slide) : variant<5, 10, 12, kPfSuffix>(arch, false);
-    if (ne <= 8) return buf ? variant<8, 4, 8, kPfBuf>(arch, slide) : variant<8, 4, 8, kPfSuffix>(arch, false);
+    if (ne <= 4) return buf ? variant<4, 10, 12, kPfBuf>(arch, slide) : variant<4, 10, 12, kPfAll>(arch, slide);
+    if (ne <= 5) return buf ? variant<5, 10, 12, kPfBuf>(arch, slide) : variant<5, 10, 12, kPfSuffix>(arch, slide);
+    if (ne <= 8) return buf ? variant<8, 4, 8, kPfBuf>(arch, slide) : variant<8, 4, 8, kPfSuffix>(arch, slide);
     return variant<16, 2, 8, kPfSuffix>(arch, false);
 }
 
@@ -914,11 +963,12 @@ int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, 
     return static_cast<int64_t>(waves) * 2 * window * stride;
 }
 
-// Word rows kept across centres (write_policy bit 3 with bit 1): skip-gram on the pipelined walk, rows
-// of 129 to 512 floats (the narrower variants measured no faster with it), and a window whose both sides
-// fit the variant's register slots.
+// Word rows kept across centres (write_policy bit 3 with bit 1): skip-gram on the pipelined walk or CBOW,
+// rows of 129 to 512 floats (the narrower variants measured no faster with it), and a window whose both
+// sides fit the variant's register slots.
 bool train_slide(int arch, int dim, bool buf, int write_policy, int window) {
-    if (arch != 0 || !buf || (write_policy & 10) != 10 || dim <= 2 * kWave || dim > 8 * kWave) return false;
+    if ((arch == 0 && !buf) || arch == 2 || (write_policy & 10) != 10 || dim <= 2 * kWave || dim > 8 * kWave)
+        return false;
     return 2 * window <= pick_variant(arch, dim, buf, true).pg;
 }
 

@@ -250,7 +250,11 @@ def test_launch_reports_need_pointers(w2v):
     (dict(dim=300, row_stride=320), dict(write_policy=15, window=6), 0),
     (dict(dim=300, row_stride=320), dict(write_policy=7), 0),
     (dict(dim=300, row_stride=320), dict(write_policy=11, cache_k=31), 0),   # cached rows not stored
-    (dict(dim=300, row_stride=320), dict(write_policy=15, arch=1), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, arch=1), 5),
+    (dict(dim=300, row_stride=320), dict(write_policy=15, arch=1, hot_k=1024), 5),
+    (dict(dim=450, row_stride=512), dict(write_policy=15, arch=1, window=5), 5),
+    (dict(dim=100, row_stride=128), dict(write_policy=15, arch=1), 0),
+    (dict(dim=300, row_stride=320), dict(write_policy=7, arch=1), 0),
     (dict(dim=300, row_stride=320), dict(write_policy=15, arch=2), 0),
     (dict(dim=300, row_stride=320), dict(write_policy=15, mode=1), 0),
     (dict(dim=300, row_stride=320), dict(write_policy=15, hot_k=8), 0),

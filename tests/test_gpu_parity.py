@@ -296,11 +296,13 @@ def test_single_worker_matches_oracle_centre_major(w2v, arch, k, F, ndocs, dim, 
     assert row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
 
 
-# write_policy 15 keeps skip-gram word rows in registers across consecutive centres (rows of 129 to 512
-# floats, window <= 5, <= 2 above 320 floats); one wavefront still reproduces the centre-major oracle. The
+# write_policy 15 keeps word rows in registers across consecutive centres (skip-gram and CBOW, rows of 129 to
+# 512 floats, window <= 5; skip-gram <= 2 above 320 floats); one wavefront still reproduces the centre-major
+# oracle. The
 # 1e3-word corpus without subsampling repeats its frequent words within most spans of ten kept positions
 # (the slots holding one word are kept equal); window 10 at dim 300 and rows of 128 floats or fewer fall
 # back to the per-centre path (the bit is ignored there).
+@pytest.mark.parametrize("arch", [0, 1])
 @pytest.mark.parametrize("name,sample,k,F,ndocs,dim,win", [
     ("sg_v30k_d100", 1e-3, 31, 10, 3, 300, 5), ("sg_v30k_d100", 1e-3, 0, 10, 3, 300, 5),
     ("sg_v30k_d100", 1e-3, 31, 1, 3, 300, 3), ("sg_v30k_d100", 1e-3, 31, 10, 3, 200, 5),
@@ -310,19 +312,21 @@ def test_single_worker_matches_oracle_centre_major(w2v, arch, k, F, ndocs, dim, 
     ("tiny_sg_v1k_d50", 0.0, 0, 10, 3, 450, 2), ("tiny_sg_v1k_d50", 0.0, 31, 10, 3, 50, 5),
     ("tiny_sg_v1k_d50", 0.0, 31, 10, 3, 150, 3), ("sg_v30k_d100", 1e-3, 31, 10, 3, 64, 5),
 ])
-def test_single_worker_word_rows_kept_across_centres(w2v, name, sample, k, F, ndocs, dim, win):
-    log(f"word rows kept across centres {name} t={sample} k={k} F={F} docs={ndocs} dim={dim} window={win}")
+def test_single_worker_word_rows_kept_across_centres(w2v, arch, name, sample, k, F, ndocs, dim, win):
+    log(f"word rows kept across centres arch={arch} {name} t={sample} k={k} F={F} docs={ndocs} dim={dim} "
+        f"window={win}")
     s = oracle_side(name)
     voc, tree = gpu_side(w2v, s)
     tv = s.tv[:ndocs * 1000]
     syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
     a0, a1 = syn0.copy(), syn1.copy()
+    alpha0 = 0.05 if arch else 0.025
     op = oracle.params(s.voc.V, dim, window=win, sample=sample, train_words=s.voc.train_words,
-                       corpus_tokens=s.tv.size, cache_k=k, flush_every=F, order=1)
+                       corpus_tokens=s.tv.size, cache_k=k, flush_every=F, order=1, arch=arch, alpha0=alpha0)
     ost = oracle.train(a0, a1, s.tree, tv, op)
     model = w2v.make_model(syn0, syn1, voc, tree)
     p = w2v.Params(window=win, sample=sample, corpus_tokens=s.tv.size, cache_k=k, flush_every=F, workers=1,
-                   write_policy=15)
+                   write_policy=15, arch=arch, alpha0=alpha0)
     st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
     assert list(st) == list(ost)
     g0, g1 = (t.cpu().numpy() for t in model.vectors())
@@ -391,6 +395,7 @@ def golden(name):
     ("sg_v100k_d200", dict(cache_mode=1)),
     ("cbow_v100k_d300", {}),
     ("cbow_v100k_d300", dict(write_policy=7)),
+    ("cbow_v100k_d300", dict(write_policy=15)),
 ])
 def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw):
     log(f"async LL {name} {kw}")
