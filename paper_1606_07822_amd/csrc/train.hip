@@ -320,6 +320,35 @@ __device__ __forceinline__ void chunk_write_delta(const TrainArgs &a, float *val
 [[maybe_unused]] constexpr int kPfNone = 0;
 constexpr int kPfAll = 1, kPfSuffix = 2, kPfBuf = 3;
 
+// One chunk of the pipelined walk: issue the loads of the next chunk (c0 + 4 ..) into nxt, fill the
+// cached rows of this chunk from LDS, update it, and store it (LDS copy or HBM).
+template <int NE, int PG>
+__device__ __forceinline__ void walk_chunk_buf(const TrainArgs &a, float *val, float (&cur)[kChunk][NE],
+                                               float (&nxt)[kChunk][NE], const float (&x)[PG][NE],
+                                               float (&e)[PG][NE], int p0, int p1, int my_pt, int c0, int len,
+                                               uint64_t code, float alpha, int lane) {
+    load_chunk_buf<NE>(nxt, a, my_pt, c0 + kChunk, len, lane);
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+        if (c0 + j < len) {
+            const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
+            if (n >= a.cache_first)
+                load_row_lds<NE>(cur[j], val + (n - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
+        }
+    }
+    const int nc = min(kChunk, len - c0);
+    chunk_update<NE, PG>(cur, x, e, p0, p1, nc, c0, code, alpha, lane);
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+        const int n = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
+        const bool live = j < nc;
+        if (live && n >= a.cache_first)
+            store_row_lds<NE>(val + (n - a.cache_first) * lds_stride<NE>(a.dim), cur[j], lane, a.dim);
+        const bool hbm = live && n < a.cache_first;
+        buf_store_row<NE>(cur[j], row_rsrc(a.syn1, hbm ? n : 0, a.stride, hbm ? a.dim * 4 : 0), lane);
+    }
+}
+
 // Walk the path of the centre with the inputs x[p0..p1) (in order), accumulating
 // the hidden-layer gradients into e[p0..p1). PG = size of the input arrays.
 template <int NE, int PG, int PF>
@@ -331,41 +360,14 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
         // Every row is written back by a store (HBM rows to HBM, cached rows into the LDS copy):
         // the pipelined walk. Each chunk issues the same memory instructions -- buffer loads of the
         // next chunk and buffer stores of this one, with empty ranges where a row is cached or past
-        // the path's end -- so the wait before a chunk's first use counts only the previous chunk's
-        // stores and the next chunk's loads stay in flight during the compute.
-        // the copy of the prefetched rows sits at the end of the loop body, behind this chunk's stores, so
-        // that its wait is counted within one iteration (a wait at the loop head would also have to cover
-        // the different order of the first chunk's loads)
-        load_chunk_buf<NE>(y0, a, my_pt, 0, len, lane);
-#pragma unroll
-        for (int j = 0; j < kChunk; ++j)
-#pragma unroll
-            for (int i = 0; i < NE; ++i) yc[j][i] = y0[j][i];
-        for (int c0 = 0; c0 < len; c0 += kChunk) {
-            load_chunk_buf<NE>(y0, a, my_pt, c0 + kChunk, len, lane);
-#pragma unroll
-            for (int j = 0; j < kChunk; ++j) {
-                if (c0 + j < len) {
-                    const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-                    if (n >= a.cache_first)
-                        load_row_lds<NE>(yc[j], val + (n - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
-                }
-            }
-            const int nc = min(kChunk, len - c0);
-            chunk_update<NE, PG>(yc, x, e, p0, p1, nc, c0, code, alpha, lane);
-#pragma unroll
-            for (int j = 0; j < kChunk; ++j) {
-                const int n = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
-                const bool live = j < nc;
-                if (live && n >= a.cache_first)
-                    store_row_lds<NE>(val + (n - a.cache_first) * lds_stride<NE>(a.dim), yc[j], lane, a.dim);
-                const bool hbm = live && n < a.cache_first;
-                buf_store_row<NE>(yc[j], row_rsrc(a.syn1, hbm ? n : 0, a.stride, hbm ? a.dim * 4 : 0), lane);
-            }
-#pragma unroll
-            for (int j = 0; j < kChunk; ++j)
-#pragma unroll
-                for (int i = 0; i < NE; ++i) yc[j][i] = y0[j][i];
+        // the path's end -- so the wait before a chunk's first use counts only the memory operations
+        // issued after its loads, and the next chunk's loads stay in flight during the compute. The two
+        // register sets take turns (the loop body walks two chunks), so no chunk is copied.
+        load_chunk_buf<NE>(yc, a, my_pt, 0, len, lane);
+        for (int c0 = 0; c0 < len; c0 += 2 * kChunk) {
+            walk_chunk_buf<NE, PG>(a, val, yc, y0, x, e, p0, p1, my_pt, c0, len, code, alpha, lane);
+            if (c0 + kChunk >= len) break;
+            walk_chunk_buf<NE, PG>(a, val, y0, yc, x, e, p0, p1, my_pt, c0 + kChunk, len, code, alpha, lane);
         }
         return;
     }
