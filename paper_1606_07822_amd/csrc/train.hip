@@ -361,13 +361,32 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
         // the pipelined walk. Each chunk issues the same memory instructions -- buffer loads of the
         // next chunk and buffer stores of this one, with empty ranges where a row is cached or past
         // the path's end -- so the wait before a chunk's first use counts only the memory operations
-        // issued after its loads, and the next chunk's loads stay in flight during the compute. The two
-        // register sets take turns (the loop body walks two chunks), so no chunk is copied.
-        load_chunk_buf<NE>(yc, a, my_pt, 0, len, lane);
-        for (int c0 = 0; c0 < len; c0 += 2 * kChunk) {
-            walk_chunk_buf<NE, PG>(a, val, yc, y0, x, e, p0, p1, my_pt, c0, len, code, alpha, lane);
-            if (c0 + kChunk >= len) break;
-            walk_chunk_buf<NE, PG>(a, val, y0, yc, x, e, p0, p1, my_pt, c0 + kChunk, len, code, alpha, lane);
+        // issued after its loads, and the next chunk's loads stay in flight during the compute.
+        if constexpr (NE == 5) {
+            // the two register sets take turns (the loop body walks two chunks), so no chunk is copied
+            // (measured faster at five elements per lane, slower at two and four, where the doubled
+            // loop body costs more than the copies)
+            load_chunk_buf<NE>(yc, a, my_pt, 0, len, lane);
+            for (int c0 = 0; c0 < len; c0 += 2 * kChunk) {
+                walk_chunk_buf<NE, PG>(a, val, yc, y0, x, e, p0, p1, my_pt, c0, len, code, alpha, lane);
+                if (c0 + kChunk >= len) break;
+                walk_chunk_buf<NE, PG>(a, val, y0, yc, x, e, p0, p1, my_pt, c0 + kChunk, len, code, alpha, lane);
+            }
+        } else {
+            // the prefetched rows are copied at the end of the loop body, behind this chunk's stores, so
+            // that their wait is counted within one iteration
+            load_chunk_buf<NE>(y0, a, my_pt, 0, len, lane);
+#pragma unroll
+            for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+                for (int i = 0; i < NE; ++i) yc[j][i] = y0[j][i];
+            for (int c0 = 0; c0 < len; c0 += kChunk) {
+                walk_chunk_buf<NE, PG>(a, val, yc, y0, x, e, p0, p1, my_pt, c0, len, code, alpha, lane);
+#pragma unroll
+                for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+                    for (int i = 0; i < NE; ++i) yc[j][i] = y0[j][i];
+            }
         }
         return;
     }
