@@ -221,6 +221,9 @@ def main():
     byte_total = (8 * d * node_rows + 8 * d * word_rows + 4 * path_len + 9 * centres
                   + n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k)
     achieved = byte_total / (kernel_ms / 1e3) / 1e9
+    # the inner-node rows alone (uncached path rows, cache fill and write-backs): the node-vector traffic
+    node_bytes = 8 * d * node_rows + n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k
+    node_gbps = node_bytes / (kernel_ms / 1e3) / 1e9
     res = w2v.last_train_resources()
     cfg_keys = {"cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
                 "write_policy": args.write_policy, "cache_mode": args.cache_mode}
@@ -266,6 +269,8 @@ def main():
         "stats": dict(zip(w2v.STAT_NAMES, map(int, st))),
         "pair_node_updates_per_s": int(st[4]) / (kernel_ms / 1e3),
         "algorithmic_bytes_per_launch": byte_total,
+        "node_vector_traffic": {"bytes_per_launch": node_bytes, "GBps": node_gbps, "frac": node_gbps / PEAK_HBM_GBS},
+        "word_span": span,
         "heldout_mean_ll": (lls[-1][0] / lls[-1][1]) if lls and lls[-1] else None,
         "cpu_baseline": cpu,
         "memory_probe": probe,
