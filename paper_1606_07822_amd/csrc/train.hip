@@ -225,7 +225,7 @@ __device__ __forceinline__ int4 centre_record(const TrainArgs &a, const int4 *re
     }
 }
 
-template <bool PATH>
+template <bool PATH, bool WV = true>
 __device__ __forceinline__ void fetch_centre(const TrainArgs &a, int4 r, const int32_t *kv, int nk, int j0, int q,
                                              int lane, int &wv, int &pt) {
     const int j = j0 + q;
@@ -233,7 +233,7 @@ __device__ __forceinline__ void fetch_centre(const TrainArgs &a, int4 r, const i
     const int lo = max(0, j - eff), hi = min(nk - 1, j + eff);
     const int c = lo + lane + ((lo + lane >= j) ? 1 : 0);
     const auto kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(kv), 0, nk * 4, kRawBufferWord3);
-    wv = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(kr, lane < hi - lo ? c * 4 : nk * 4, 0, 0));
+    if constexpr (WV) wv = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(kr, lane < hi - lo ? c * 4 : nk * 4, 0, 0));
     if constexpr (PATH) {
         const int po = __builtin_amdgcn_readfirstlane(r.z), len = __builtin_amdgcn_readfirstlane(r.w);
         const auto pr = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(a.points) + po, 0, len * 4,
@@ -468,14 +468,14 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
 // kept equal: a change made to one is added to the others, and a word entering the span is copied
 // from a slot that holds it rather than read from memory.
 template <int PG>
-__device__ __forceinline__ bool span_has_dup(int sid, int lane) {
-    uint64_t any = 0;
+__device__ __forceinline__ int span_pairs(int sid, int lane) {
+    int n = 0;
 #pragma unroll
     for (int q = 0; q < PG - 1; ++q) {
         const int w = __builtin_amdgcn_readlane(sid, q);
-        any |= __ballot(w >= 0 && lane > q && lane < PG && sid == w);
+        n += __popcll(__ballot(w >= 0 && lane > q && lane < PG && sid == w));
     }
-    return any != 0;
+    return n;
 }
 
 // Row of slot q from memory (zeros when the slot lies outside the document).
@@ -495,9 +495,10 @@ __device__ __forceinline__ void span_store(const float (&xw)[PG][NE], int q, con
 // that holds w, else the row from memory. Returns the slot's dirty bit.
 template <int NE, int PG, int DST>
 __device__ __forceinline__ uint32_t span_enter(float (&xw)[PG][NE], const TrainArgs &a, int sid, uint32_t dirty,
-                                               int lane) {
+                                               int &pairs, int lane) {
     const int w = __builtin_amdgcn_readlane(sid, DST);
     const uint64_t m = w >= 0 ? __ballot(lane < PG - 1 && lane != DST && sid == w) : 0ull;
+    pairs += __popcll(m);
     if (m == 0ull) {
         span_load<NE, PG>(xw, DST, a, sid, lane);
         return 0u;
@@ -580,11 +581,16 @@ __device__ __forceinline__ void span_apply_same(float (&xw)[PG][NE], const float
 // word v and slot PG-1 the word at position j+1+H (w_edge, -1 past the document's end).
 template <int NE, int PG>
 __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs &a, int &sid, uint32_t &dirty,
-                                           bool &dup, int v, int w_edge, int lane) {
+                                           int &pairs, int v, int w_edge, int lane) {
     constexpr int H = PG / 2;
     constexpr uint32_t low = (1u << (H - 1)) - 1u;
     if (dirty & 1u) span_store<NE, PG>(xw, 0, a, sid, lane);
     if ((dirty >> H) & 1u) span_store<NE, PG>(xw, H, a, sid, lane);
+    if (pairs > 0) {   // equal pairs that slots 0 and H leave behind
+        const int w0 = __builtin_amdgcn_readlane(sid, 0), wh = __builtin_amdgcn_readlane(sid, H);
+        pairs -= w0 >= 0 ? __popcll(__ballot(lane > 0 && lane < PG && sid == w0)) : 0;
+        pairs -= wh >= 0 ? __popcll(__ballot(lane != 0 && lane != H && lane < PG && sid == wh)) : 0;
+    }
 #pragma unroll
     for (int q = 0; q + 1 < H; ++q)
 #pragma unroll
@@ -597,9 +603,8 @@ __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs 
     const int src = (lane < H - 1 || (lane >= H && lane < PG - 1)) ? lane + 1 : lane;
     sid = __shfl(sid, src, kWave);
     sid = lane == H - 1 ? v : (lane == PG - 1 ? w_edge : sid);
-    dirty |= span_enter<NE, PG, H - 1>(xw, a, sid, dirty, lane) << (H - 1);
-    dirty |= span_enter<NE, PG, PG - 1>(xw, a, sid, dirty, lane) << (PG - 1);
-    dup = span_has_dup<PG>(sid, lane);
+    dirty |= span_enter<NE, PG, H - 1>(xw, a, sid, dirty, pairs, lane) << (H - 1);
+    dirty |= span_enter<NE, PG, PG - 1>(xw, a, sid, dirty, pairs, lane) << (PG - 1);
 }
 
 
@@ -668,19 +673,19 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
             }
             int wv_next = 0, pt_next = 0;
-            fetch_centre<ARCH != 2>(a, centre_record<kRec>(a, rec, kv, km, j0, 0), kv, nk, j0, 0, lane, wv_next,
+            fetch_centre<ARCH != 2, !SLIDE>(a, centre_record<kRec>(a, rec, kv, km, j0, 0), kv, nk, j0, 0, lane, wv_next,
                                     pt_next);
             constexpr int H = PG / 2;
             float xw[SLIDE ? PG : 1][NE];
             int sid = -1;
             uint32_t dirty = 0;
-            bool dup = false;
+            int pairs = 0;   // slot pairs holding the same word
             if constexpr (SLIDE) {
                 const int pos = lane < H ? j0 - H + lane : j0 + 1 + lane - H;
                 sid = (lane < PG && pos >= 0 && pos < nk) ? kv[pos] : -1;
 #pragma unroll
                 for (int q = 0; q < PG; ++q) span_load<NE, PG>(xw, q, a, sid, lane);
-                dup = span_has_dup<PG>(sid, lane);
+                pairs = span_pairs<PG>(sid, lane);
             }
             for (int j = j0; j < j1; ++j) {
                 const int4 r = centre_record<kRec>(a, rec, kv, km, j0, j - j0);
@@ -691,7 +696,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                 int wv = wv_next, my_pt = pt_next;
                 asm volatile("" : "+v"(wv), "+v"(my_pt));   // one wait for the fetched values here, none at their uses
                 const int qn = min(j + 1, j1 - 1) - j0;
-                fetch_centre<ARCH != 2>(a, centre_record<kRec>(a, rec, kv, km, j0, qn), kv, nk, j0, qn, lane, wv_next,
+                fetch_centre<ARCH != 2, !SLIDE>(a, centre_record<kRec>(a, rec, kv, km, j0, qn), kv, nk, j0, qn, lane, wv_next,
                                         pt_next);
                 const int eff = static_cast<int>(meta >> 16);
                 const int lo = max(0, j - eff), hi = min(nk - 1, j + eff);
@@ -720,7 +725,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
 #pragma unroll
                         for (int i = 0; i < NE; ++i) h[0][i] = h[0][i] / fP;
                         walk_path<NE, 1, PF>(a, val, h, e, 0, 1, my_pt, len, code, alpha, lane);
-                        span_apply_same<NE, PG>(xw, e[0], p0, p1, sid, dup, dirty, lane);
+                        span_apply_same<NE, PG>(xw, e[0], p0, p1, sid, pairs > 0, dirty, lane);
                         n_nodes += len;
                     } else if constexpr (SLIDE) {
                         const int p0 = H - (j - lo), p1 = H + (hi - j);
@@ -728,7 +733,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
 #pragma unroll
                         for (int q = 0; q < PG; ++q) zero_row<NE>(e[q]);
                         walk_path<NE, PG, PF>(a, val, xw, e, p0, p1, my_pt, len, code, alpha, lane);
-                        span_apply<NE, PG>(xw, e, p0, p1, sid, dup, dirty, lane);
+                        span_apply<NE, PG>(xw, e, p0, p1, sid, pairs > 0, dirty, lane);
                         n_nodes += static_cast<uint64_t>(P) * len;
                     } else if constexpr (ARCH == 0) {
                         // groups of PG window words walk the path in turn (one group when P <= PG). With
@@ -874,7 +879,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     }
                 }
                 if constexpr (SLIDE) {
-                    if (j + 1 < j1) span_shift<NE, PG>(xw, a, sid, dirty, dup, v, w_edge, lane);
+                    if (j + 1 < j1) span_shift<NE, PG>(xw, a, sid, dirty, pairs, v, w_edge, lane);
                 }
             }
             if constexpr (SLIDE) {
