@@ -166,7 +166,7 @@ def test_full_sync_first_batches_within_1e4(w2v, batches, B):
     np.testing.assert_array_equal(g1[:ov.V - 1][~touched1], syn1[~touched1])
 
 
-@pytest.mark.parametrize("k,wp", [(31, 5), (31, 0), (0, 1)])
+@pytest.mark.parametrize("k,wp", [(31, 5), (31, 0), (0, 1), (31, 15), (0, 11)])
 def test_full_single_worker_matches_oracle_centre_major(w2v, k, wp):
     log(f"full-size single worker k={k} write_policy={wp}")
     w, _, ov, ot = oracle_full()
