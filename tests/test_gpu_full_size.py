@@ -118,9 +118,10 @@ def test_full_epoch_in_bench_launch(w2v):
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
     s0, npairs, nnodes = w2v.hs_loglik(model, held, pe)
     assert abs(s0 + math.log(2.0) * nnodes) <= 1e-9 * nnodes      # syn1 = 0: every node gives log(1/2)
-    # bench.py's settings: every row stored (write_policy 7)
+    # bench.py's settings: every row stored, word rows kept across centres (write_policy 15)
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
-                   seed=synth.SEED_TRAIN, write_policy=7)
+                   seed=synth.SEED_TRAIN, write_policy=15)
+    assert w2v.train_word_span(model, p) == 5
     st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
     grid, waves = w2v.last_train_launch()
     log(f"  launch {grid} workgroups, {waves} wavefronts, {w2v.last_train_kernel_ms():.0f} ms")
