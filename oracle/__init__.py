@@ -27,7 +27,8 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# W2V_ORACLE_LIB names another build of the same source (e.g. one made with -march=native).
+LIB_PATH = os.environ.get("W2V_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 SRC_PATH = os.path.join(_HERE, "w2v_oracle.c")
 
 P = ctypes.c_void_p
@@ -50,7 +51,7 @@ def build(force: bool = False) -> str:
     """Compile liboracle.so with gcc (plain C, no FMA contraction)."""
     import subprocess
     if force or not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(SRC_PATH):
-        subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off", "-fPIC",
+        subprocess.check_call(["gcc", "-O3", "-march=x86-64-v3", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off", "-fPIC",
                                "-shared", SRC_PATH, "-o", LIB_PATH, "-lm"])
     return LIB_PATH
 
@@ -286,7 +287,12 @@ def log_prob(x: np.ndarray, syn1: np.ndarray, tree: Tree, v: int) -> float:
 
 
 def loglik(syn0: np.ndarray, syn1: np.ndarray, tree: Tree, tokens_v: np.ndarray, p: Params):
-    """(sum of log P(v|w) over the sampler's pairs, n_pairs, n_nodes)."""
+    """(sum of the held-out objective, n_terms, n_nodes).
+
+    p.arch 0: log P(v|w) summed over the sampler's pairs (v, w).
+    p.arch 1 (CBOW): log P(v|h) summed over the sampler's centres that have a
+    window, h = the mean of the window words' vectors.
+    """
     tok = np.ascontiguousarray(tokens_v, dtype=np.int32)
     s = ctypes.c_double(0)
     npairs = ctypes.c_int64(0)

@@ -642,9 +642,30 @@ double or_log_prob(const float *x, const float *syn1, int32_t dim, const or_tree
     return s;
 }
 
+/* log P(v | h) for an fp64 input h and fp32 inner-node vectors. */
+static double or_log_prob_mixed(const double *h, const float *syn1, int32_t dim, const or_tree *t, int32_t v) {
+    double s = 0.0;
+    const int32_t *pts = t->points + t->point_off[v];
+    for (int32_t j = 0; j < t->codelen[v]; j++) {
+        const float *y = syn1 + (size_t)pts[j] * dim;
+        double z = 0.0;
+        for (int32_t k = 0; k < dim; k++) z += h[k] * (double)y[k];
+        double sign = ((t->code[v] >> j) & 1u) ? -1.0 : 1.0;
+        s += log_sigmoid(sign * z);
+    }
+    return s;
+}
+
 /*
- * Sum over the sampler's pairs (v, w) of log P(v | vector[w]); the pairs are
- * drawn with p's seed, epoch and sampling settings (R11-R13).
+ * Held-out objective of the sampler's stream, drawn with p's seed, epoch and
+ * sampling settings (R11-R13).
+ * arch 0 (skip-gram): the sum over pairs (v, w) of log P(v | vector[w]);
+ *   n_pairs counts pairs.
+ * arch 1 (CBOW): the sum over centres v with at least one window word of
+ *   log P(v | h), h = the mean of the window words' vectors (taken in fp64),
+ *   the same hierarchical softmax (§2) with CBOW's input; n_pairs counts those
+ *   centres.
+ * n_nodes: the tree nodes the terms visit.
  */
 int or_loglik(const float *syn0, const float *syn1, const or_tree *t, const int32_t *tokens, int64_t n,
               const or_params *p, double *sum_ll, int64_t *n_pairs, int64_t *n_nodes) {
@@ -654,12 +675,26 @@ int or_loglik(const float *syn0, const float *syn1, const or_tree *t, const int3
     if (!thr) return -1;
     or_keep_thresholds(t->vocab_counts, p->V, p->sample, p->train_words, thr);
     int32_t ctx[2 * 1024 + 2];
+    double *h = (double *)malloc(sizeof(double) * (size_t)p->dim);
+    if (!h) return -1;
     int64_t inv = 0, np = 0, nn = 0;
     double s = 0.0;
     for (int64_t lo = 0; lo < n; lo += p->doc_len) {
         doc_sample(tokens, n, p, thr, lo, &d, &inv);
         for (int32_t j = 0; j < d.n; j++) {
             int32_t m = window_of(&d, j, ctx);
+            if (p->arch == 1) {
+                if (m == 0) continue;
+                for (int32_t k = 0; k < p->dim; k++) {
+                    double a = 0.0;
+                    for (int32_t q = 0; q < m; q++) a += (double)syn0[(size_t)d.vid[ctx[q]] * p->dim + k];
+                    h[k] = a / (double)m;
+                }
+                s += or_log_prob_mixed(h, syn1, p->dim, t, d.vid[j]);
+                np++;
+                nn += t->codelen[d.vid[j]];
+                continue;
+            }
             for (int32_t q = 0; q < m; q++) {
                 s += or_log_prob(syn0 + (size_t)d.vid[ctx[q]] * p->dim, syn1, p->dim, t, d.vid[j]);
                 np++;
@@ -672,6 +707,7 @@ int or_loglik(const float *syn0, const float *syn1, const or_tree *t, const int3
     if (n_nodes) *n_nodes = nn;
     doc_free(&d);
     free(thr);
+    free(h);
     return 0;
 }
 

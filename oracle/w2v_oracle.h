@@ -84,6 +84,8 @@ int or_train_sync(float *syn0, float *syn1, const or_tree *t, const int32_t *tok
 /* ---- evaluation ---- */
 double or_log_prob(const float *x, const float *syn1, int32_t dim, const or_tree *t, int32_t v);
 double or_log_prob_f64(const double *x, const double *syn1, int32_t dim, const or_tree *t, int32_t v);
+/* p->arch 0: sum of log P(v | vector[w]) over the sampled pairs; p->arch 1 (CBOW): sum of log P(v | h)
+   over the sampled centres with a window, h = the mean of the window vectors. n_pairs counts the terms. */
 int or_loglik(const float *syn0, const float *syn1, const or_tree *t, const int32_t *tokens, int64_t n,
               const or_params *p, double *sum_ll, int64_t *n_pairs, int64_t *n_nodes);
 

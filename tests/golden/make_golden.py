@@ -61,7 +61,7 @@ def run(name: str, cache_k: int = 31, flush_every: int = 10, train_tokens: int =
     hv = oracle.remap(held, voc.id_to_vocab)
     syn0, syn1 = synth.init_weights(voc.V, w.dim)
     pe = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, train_words=voc.train_words,
-                       seed=synth.SEED_EVAL)
+                       seed=synth.SEED_EVAL, arch=w.arch)
     s0, npairs, _ = oracle.loglik(syn0, syn1, tree, hv, pe)
     t1 = time.time()
     stats = []

@@ -2,7 +2,10 @@
 
 What fixes these other than the oracle itself:
   * the hierarchical softmax is a distribution: sum_v P(v|x) = 1 (fp64);
-  * log-likelihood at syn1 = 0 is -ln 2 per node (closed form);
+  * log-likelihood at syn1 = 0 is -ln 2 per node (closed form), for the
+    pairs' objective and for CBOW's;
+  * CBOW's objective equals log P(v|h) of the softmax above with h the mean
+    of the materialised context rows of each centre (rebuilt in numpy);
   * one update of Algorithm 1 equals alpha times the gradient of log P(v|w),
     by central finite differences (skip-gram, CBOW, synchronous mode);
   * from syn1 = 0 one pair gives syn1[n_j] = alpha (1/2 - t_j) x_w and leaves
@@ -56,6 +59,50 @@ def test_loglik_at_zero_syn1_is_minus_ln2_per_node():
     s, npairs, nnodes = oracle.loglik(syn0, syn1, tree, tv, p)
     assert npairs > 0
     assert abs(s - (-math.log(2.0) * nnodes)) < 1e-6 * nnodes
+
+
+def test_cbow_loglik_at_zero_syn1_is_minus_ln2_per_node():
+    w = synth.WORKLOADS["tiny_sg_v1k_d50"]
+    tok = synth.workload_corpus(w)
+    voc = oracle.build_vocab(tok, w.vocab, w.min_count)
+    tree = oracle.build_huffman(voc.vocab_counts)
+    tv = oracle.remap(tok, voc.id_to_vocab)
+    syn0, syn1 = synth.init_weights(voc.V, w.dim)
+    p = oracle.params(voc.V, w.dim, window=w.window, train_words=voc.train_words, seed=4, arch=1)
+    s, ncentres, nnodes = oracle.loglik(syn0, syn1, tree, tv, p)
+    assert ncentres > 0
+    assert nnodes == int(tree.codelen[tv].astype(np.int64).sum())     # every centre has a window here
+    assert abs(s - (-math.log(2.0) * nnodes)) < 1e-6 * nnodes
+
+
+@pytest.mark.parametrize("window,sample", [(2, 0.0), (5, 1e-2)])
+def test_cbow_loglik_is_log_prob_of_the_window_mean(window, sample):
+    """CBOW's objective, rebuilt from the materialised pairs: per centre, h = the mean of its context
+    rows (numpy, fp64), scored with the softmax whose normalisation is pinned above."""
+    w = synth.WORKLOADS["tiny_sg_v1k_d50"]
+    tok = synth.workload_corpus(w)[:8000]
+    voc = oracle.build_vocab(tok, w.vocab, 1)
+    tree = oracle.build_huffman(voc.vocab_counts)
+    tv = oracle.remap(tok, voc.id_to_vocab)
+    rng = np.random.default_rng(7)
+    syn0 = ((rng.random((voc.V, w.dim)) - 0.5) * 0.6).astype(np.float32)
+    syn1 = ((rng.random((voc.V - 1, w.dim)) * 2 - 1) * 0.3).astype(np.float32)
+    p = oracle.params(voc.V, w.dim, window=window, sample=sample, train_words=voc.train_words, seed=4, arch=1)
+    s, ncentres, nnodes = oracle.loglik(syn0, syn1, tree, tv, p)
+    pr = oracle.sample_pairs(tv, p, voc.vocab_counts)
+    s1 = syn1.astype(np.float64)
+    ref, centres = 0.0, 0
+    for c in np.unique(pr.centre):
+        ctx = pr.context[pr.centre == c]
+        h = syn0[tv[ctx]].astype(np.float64).mean(axis=0)
+        ref += oracle.log_prob(h, s1, tree, int(tv[c]))
+        centres += 1
+    assert ncentres == centres > 100
+    assert abs(s - ref) <= 1e-12 * abs(ref)
+    # the skip-gram objective on the same stream is a different number (one term per pair)
+    p0 = oracle.params(voc.V, w.dim, window=window, sample=sample, train_words=voc.train_words, seed=4)
+    s0, npairs, _ = oracle.loglik(syn0, syn1, tree, tv, p0)
+    assert npairs == pr.total > ncentres and abs(s0 - s) > 1.0
 
 
 # ------------------------------------------------------- one-pair updates
