@@ -10,18 +10,25 @@ The JSON line also carries the roofline of the training kernel (algorithmic
 bytes per launch from the byte model below, over the kernel's duration timed
 with HIP events on its stream) and the CPU oracle's rate on a bounded sample.
 
-Byte model, per kept centre v with P > 0 window words (fp32 rows of d floats):
+Byte model (roofline.achieved), per kept centre v with P > 0 window words
+(fp32 rows of d floats):
     8 d (len(v) - cached(v))   inner-node rows read and written once
   + 8 d P                      window rows read once and updated once
   + 4 len(v) + 9               path indices, code, length
 plus the cache traffic of each workgroup: fill 4 d k, write-back 8 d k per
-flush and at the end. When the word rows of a span of H kept positions on
-each side of the centre stay in registers across centres (write_policy bit 3),
-the 8 d P term becomes 8 d per row entering a span: per work unit (a segment of
-consecutive kept centres j0 .. j1-1 of a document with nk kept words) the
-rows of its first centre's span, then per later centre the previous centre's
-row and the row H positions ahead when it exists; each is read once and
-written back once.
+flush and at the end.
+
+Span model (span_model, reported beside it): when the word rows of a span of
+H kept positions on each side of the centre stay in registers across centres
+(write_policy bit 3), the 8 d P term becomes 8 d per row entering a span: per
+work unit (a segment of consecutive kept centres j0 .. j1-1 of a document
+with nk kept words) the rows of its first centre's span, then per later
+centre the previous centre's row and the row H positions ahead when it
+exists; each is read once and written back once. It is the smaller count, so
+its fraction of the peak is the stricter one.
+
+With --cpu-child DIR the script is instead the CPU baseline's pinned child
+process (see cpu_baseline).
 """
 from __future__ import annotations
 
@@ -121,6 +128,7 @@ def main():
     import numpy as np
     import torch
 
+    import bench_probe
     import paper_1606_07822_amd as w2v
     import synth
 
@@ -147,9 +155,10 @@ def main():
                    seed=synth.SEED_TRAIN, cache_k=args.cache_k, flush_every=args.flush_every,
                    flush_policy=args.flush_policy, write_policy=args.write_policy, workers=args.workers,
                    cache_mode=args.cache_mode)
-    pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
+    pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL, arch=w.arch)
     # held-out tokens as vocabulary indices (input preparation; the vocabulary is the same every step)
     held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
+    ll_init = None if args.no_loglik else w2v.hs_loglik(model, held, pe)
     ws = torch.empty(w2v.train_workspace_bytes(model, w.n_tokens, p), dtype=torch.uint8, device=dev)
     stats = torch.zeros(w2v.N_STATS, dtype=torch.int64, device=dev)
 
@@ -164,8 +173,8 @@ def main():
         rows, cols = 1_000_000, 320
         m = torch.empty(rows, cols, dtype=torch.float32, device=dev)
         iters = -(-rows // (256 * 12 * 4))
-        w2v.probe_rows(m, cols, 3, 256, iters)
-        w2v.probe_rows(m, cols, 2, 256, iters)
+        bench_probe.probe_rows(m, cols, 3, 256, iters)
+        bench_probe.probe_rows(m, cols, 2, 256, iters)
         torch.cuda.synchronize()
         del m
         calib = {"rows": rows, "row_bytes": 4 * cols, "write_dispatch": "k_probe<3, 5>", "read_dispatch": "k_probe<2, 5>"}
@@ -218,9 +227,13 @@ def main():
     d = w.dim
     n_groups, n_waves = w2v.last_train_launch()
     flushes = centres // max(1, args.flush_every) + n_groups
-    byte_total = (8 * d * node_rows + 8 * d * word_rows + 4 * path_len + 9 * centres
-                  + n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k)
-    achieved = byte_total / (kernel_ms / 1e3) / 1e9
+    cache_bytes = n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k
+    # the per-centre byte model B(v): every window word's row read and updated once per pair (8 d P)
+    byte_model = 8 * d * node_rows + 8 * d * pairs + 4 * path_len + 9 * centres + cache_bytes
+    # the tighter count for a kernel that keeps word rows across centres: 8 d per row entering a span
+    byte_span = 8 * d * node_rows + 8 * d * word_rows + 4 * path_len + 9 * centres + cache_bytes
+    achieved = byte_model / (kernel_ms / 1e3) / 1e9
+    achieved_span = byte_span / (kernel_ms / 1e3) / 1e9
     # the inner-node rows alone (uncached path rows, cache fill and write-backs): the node-vector traffic
     node_bytes = 8 * d * node_rows + n_groups * 4 * d * args.cache_k + flushes * 8 * d * args.cache_k
     node_gbps = node_bytes / (kernel_ms / 1e3) / 1e9
@@ -234,6 +247,16 @@ def main():
         t = json.load(open(tfile))
         if t.get("kernel_source") == w2v.kernel_source_hash() and t.get("settings") == cfg_keys:
             traffic = t.get("hbm_bytes_per_launch")
+
+    # learning achieved against the sequential oracle's full epoch on the same workload, when stored:
+    # (init - gpu) / (init - oracle) of the held-out mean log-likelihood
+    ll_final = (lls[-1][0] / lls[-1][1]) if lls and lls[-1] else None
+    oracle_ll = gain_frac = None
+    gfile = os.path.join(ROOT, "tests", "golden", f"oracle_ll_{args.workload}.json")
+    if ll_final is not None and ll_init and os.path.exists(gfile):
+        g = json.load(open(gfile))
+        oracle_ll = g["mean_ll"]
+        gain_frac = (ll_final - ll_init[0] / ll_init[1]) / (oracle_ll - g["init_mean_ll"])
 
     # the training kernel moves whole padded rows (row_stride >= 64 * ceil(d / 64) floats) when it can
     share = 64 * (-(-d // 64))
@@ -268,10 +291,17 @@ def main():
         "train_kernel_words_per_s": words / (kernel_ms / 1e3),
         "stats": dict(zip(w2v.STAT_NAMES, map(int, st))),
         "pair_node_updates_per_s": int(st[4]) / (kernel_ms / 1e3),
-        "algorithmic_bytes_per_launch": byte_total,
+        "algorithmic_bytes_per_launch": byte_model,
+        "byte_model_terms": {"node_rows": node_rows, "pairs": pairs, "path_nodes": path_len, "centres": centres,
+                             "span_word_rows": word_rows, "cache_fill_and_writeback_bytes": cache_bytes,
+                             "dim": d, "workgroups": n_groups, "flushes": flushes},
+        "span_model": {"bytes_per_launch": byte_span, "GBps": achieved_span, "frac": achieved_span / PEAK_HBM_GBS},
         "node_vector_traffic": {"bytes_per_launch": node_bytes, "GBps": node_gbps, "frac": node_gbps / PEAK_HBM_GBS},
         "word_span": span,
-        "heldout_mean_ll": (lls[-1][0] / lls[-1][1]) if lls and lls[-1] else None,
+        "heldout_mean_ll": ll_final,
+        "heldout_init_mean_ll": (ll_init[0] / ll_init[1]) if ll_init else None,
+        "oracle_mean_ll": oracle_ll,
+        "gain_fraction_vs_oracle": gain_frac,
         "cpu_baseline": cpu,
         "memory_probe": probe,
         "counter_calibration": calib,
@@ -346,7 +376,7 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
     achieved = byte_total / (kernel_ms / 1e3) / 1e9
     n_groups, n_waves = w2v.last_train_launch()
     res = w2v.last_train_resources()
-    cpu = None if args.no_cpu_baseline else cpu_baseline_ns(w, tok_np, args, K)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w, tok_np, args, negative=K)
     line = {
         "metric": f"trained words/sec, skip-gram with {K} shared negatives V=1M d=300 fp32; % of HBM roofline",
         "value": words / (ms_per_step / 1e3),
@@ -376,35 +406,6 @@ def ns_main(args, torch, w2v, synth, w, tok, tok_np, held_np, dev):
         "launch": {"workgroups": n_groups, "wavefronts": n_waves, **res},
     }
     print(json.dumps(line), flush=True)
-
-
-def cpu_baseline_ns(w, tok_np, args, K):
-    """The oracle's shared-negative training on a prefix of the same corpus, timed on this host."""
-    import numpy as np
-    import oracle
-    import synth
-    voc = oracle.build_vocab(tok_np, w.vocab, w.min_count)
-    L = max(10, min(27, (64 * voc.V - 1).bit_length()))
-    table = oracle.noise_table(voc.vocab_counts, L)
-    p = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, alpha0=w.alpha0, train_words=voc.train_words,
-                      corpus_tokens=w.n_tokens, seed=synth.SEED_TRAIN, negative=K)
-    syn0, _ = synth.init_weights(voc.V, w.dim)
-    syn1 = np.zeros((voc.V, w.dim), np.float32)
-    oracle.train_ns(syn0, syn1, voc.vocab_counts, table, L, oracle.remap(tok_np[:2 * w.doc_len], voc.id_to_vocab), p)
-    n_cal = 20 * w.doc_len
-    tv = oracle.remap(tok_np[:n_cal], voc.id_to_vocab)
-    t0 = time.perf_counter()
-    oracle.train_ns(syn0, syn1, voc.vocab_counts, table, L, tv, p)
-    per_tok = (time.perf_counter() - t0) / n_cal
-    n = int(min(w.n_tokens, max(n_cal, args.cpu_seconds / max(per_tok, 1e-9))))
-    n = (n // w.doc_len) * w.doc_len or n_cal
-    tv = oracle.remap(tok_np[:n], voc.id_to_vocab)
-    t0 = time.perf_counter()
-    st = oracle.train_ns(syn0, syn1, voc.vocab_counts, table, L, tv, p)
-    dt = time.perf_counter() - t0
-    return {"value": float(st[1]) / dt, "unit": "words/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {n:,} tokens ({n // w.doc_len} documents) of the same corpus, one epoch of "
-                      f"shared-negative training (K={K}), {dt:.1f}s on one host core"}
 
 
 def sweep_cache(args, torch, w2v, synth, w, voc, tree, model, held, pe, ws, stats):
@@ -443,6 +444,7 @@ def sweep_cache(args, torch, w2v, synth, w, voc, tree, model, held, pe, ws, stat
 
 
 def memory_probe(torch, w2v, rows, cols, stride, dev):
+    import bench_probe
     """Practical memory ceiling of the training kernel's access pattern: rows of
     cols floats (the padded row the kernel moves; rows = V) at hashed positions,
     four in flight per wavefront on the same launch shape, read and
@@ -452,8 +454,8 @@ def memory_probe(torch, w2v, rows, cols, stride, dev):
     visits = wg * 12 * 4 * iters
     out = {"rows": rows, "row_bytes": 4 * cols, "row_visits": visits}
     for mode, name in ((0, "read"), (1, "rmw")):
-        w2v.probe_rows(m, cols, mode, wg, iters)                 # warm-up
-        ms = w2v.probe_rows(m, cols, mode, wg, iters)
+        bench_probe.probe_rows(m, cols, mode, wg, iters)                 # warm-up
+        ms = bench_probe.probe_rows(m, cols, mode, wg, iters)
         moved = visits * 4 * cols * (2 if mode else 1)
         out[f"{name}_GBps"] = moved / (ms / 1e3) / 1e9
         out[f"{name}_rows_per_s"] = visits / (ms / 1e3)
@@ -462,38 +464,128 @@ def memory_probe(torch, w2v, rows, cols, stride, dev):
     return out
 
 
-def cpu_baseline(w, tok_np, args):
-    """The oracle (single-threaded C) on a prefix of the same corpus, timed on this host."""
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(w, tok_np, args, negative=0):
+    """The oracle (single-threaded C) on a prefix of the same corpus, timed on this host.
+
+    The oracle is compiled for this host (gcc -O3 -march=native -ffp-contract=off) into a temporary
+    directory, and the timed run is a child process pinned to one core with taskset, which reads the
+    vocabulary counts and the token prefix from that directory: nothing else runs on that core, and
+    the GPU process is not involved.
+    """
+    import shutil
+    import subprocess
+    import tempfile
+
+    import numpy as np
+
+    import oracle
+
+    t0 = time.time()
+    voc = oracle.build_vocab(tok_np, w.vocab, w.min_count)
+    log(f"oracle vocabulary in {time.time() - t0:.1f}s")
+    tmp = tempfile.mkdtemp(prefix="w2v_cpu_")
+    try:
+        n_pre = min(w.n_tokens, 16_000 * w.doc_len)
+        np.save(os.path.join(tmp, "vocab_counts.npy"), voc.vocab_counts)
+        np.save(os.path.join(tmp, "tokens.npy"), oracle.remap(tok_np[:n_pre], voc.id_to_vocab))
+        with open(os.path.join(tmp, "job.json"), "w") as f:
+            json.dump({"workload": w.name, "train_words": voc.train_words, "negative": negative,
+                       "cpu_seconds": args.cpu_seconds}, f)
+        lib = os.path.join(tmp, "liboracle_native.so")
+        build = ["gcc", "-O3", "-march=native", "-std=c11", "-ffp-contract=off", "-fPIC", "-shared",
+                 oracle.SRC_PATH, "-o", lib, "-lm"]
+        env = dict(os.environ)
+        try:
+            subprocess.run(build, check=True, capture_output=True)
+            env["W2V_ORACLE_LIB"] = lib
+            build_s = "gcc -O3 -march=native -ffp-contract=off (single-threaded C)"
+        except (OSError, subprocess.CalledProcessError):
+            build_s = "the committed liboracle.so (gcc -O3 -march=x86-64-v3 -ffp-contract=off); native build failed"
+        cores = sorted(os.sched_getaffinity(0))
+        core = cores[-1]
+        cmd = [sys.executable, os.path.abspath(__file__), "--cpu-child", tmp]
+        pin = None
+        if shutil.which("taskset"):
+            cmd = ["taskset", "-c", str(core)] + cmd
+            pin = f"taskset -c {core}"
+        r = subprocess.run(cmd, env=env, capture_output=True, text=True, timeout=600)
+        if r.returncode != 0:
+            log(f"CPU baseline child failed: {r.stderr[-2000:]}")
+            return None
+        out = json.loads(r.stdout.strip().splitlines()[-1])
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    out.update({"unit": "words/s", "cores": 1, "kind": "oracle", "cpu_model": _cpu_model(),
+                "nproc": os.cpu_count(), "cores_allowed": len(cores), "pinned": pin, "build": build_s})
+    return out
+
+
+def cpu_child(tmp):
+    """Child process of cpu_baseline: calibrate on 20 documents, then time about cpu_seconds of training."""
     import numpy as np
 
     import oracle
     import synth
 
-    t0 = time.time()
-    voc = oracle.build_vocab(tok_np, w.vocab, w.min_count)
-    tree = oracle.build_huffman(voc.vocab_counts)
-    log(f"oracle vocabulary + tree in {time.time() - t0:.1f}s")
-    syn0, syn1 = synth.init_weights(voc.V, w.dim)
-    # calibrate on 20 documents (after 2 that warm the pages up), then size the sample to about cpu_seconds
-    p = oracle.params(voc.V, w.dim, window=w.window, sample=w.sample, alpha0=w.alpha0, train_words=voc.train_words,
-                      corpus_tokens=w.n_tokens, seed=synth.SEED_TRAIN, cache_k=31, flush_every=10, arch=w.arch)
-    oracle.train(syn0, syn1, tree, oracle.remap(tok_np[:2 * w.doc_len], voc.id_to_vocab), p)
-    n_cal = 20 * w.doc_len
-    tv = oracle.remap(tok_np[:n_cal], voc.id_to_vocab)
+    job = json.load(open(os.path.join(tmp, "job.json")))
+    w = synth.WORKLOADS[job["workload"]]
+    vc = np.load(os.path.join(tmp, "vocab_counts.npy"))
+    tv_all = np.load(os.path.join(tmp, "tokens.npy"))
+    V, K = int(vc.size), int(job["negative"])
+    p = oracle.params(V, w.dim, window=w.window, sample=w.sample, alpha0=w.alpha0, train_words=job["train_words"],
+                      corpus_tokens=w.n_tokens, seed=synth.SEED_TRAIN, cache_k=31, flush_every=10, arch=w.arch,
+                      negative=K if K else 5)
+    if K:
+        L = max(10, min(27, (64 * V - 1).bit_length()))
+        table = oracle.noise_table(vc, L)
+
+        def fresh():
+            s0, _ = synth.init_weights(V, w.dim)
+            return s0, np.zeros((V, w.dim), np.float32)
+
+        def run(s0, s1, tv):
+            return oracle.train_ns(s0, s1, vc, table, L, tv, p)
+        what = f"one epoch of shared-negative training (K={K})"
+    else:
+        tree = oracle.build_huffman(vc)
+
+        def fresh():
+            return synth.init_weights(V, w.dim)
+
+        def run(s0, s1, tv):
+            return oracle.train(s0, s1, tree, tv, p)
+        what = "one epoch of Algorithm 1 with the top-31 cache flushed every 10 centres (u=10)"
+    syn0, syn1 = fresh()
+    run(syn0, syn1, tv_all[:2 * w.doc_len])                     # warms the pages up
+    n_cal = min(tv_all.size, 20 * w.doc_len)
     t0 = time.perf_counter()
-    oracle.train(syn0, syn1, tree, tv, p)
+    run(syn0, syn1, tv_all[:n_cal])
     per_tok = (time.perf_counter() - t0) / n_cal
-    n = int(min(w.n_tokens, max(n_cal, args.cpu_seconds / max(per_tok, 1e-9))))
+    n = int(min(tv_all.size, max(n_cal, job["cpu_seconds"] / max(per_tok, 1e-9))))
     n = (n // w.doc_len) * w.doc_len or n_cal
-    syn0, syn1 = synth.init_weights(voc.V, w.dim)
-    tv = oracle.remap(tok_np[:n], voc.id_to_vocab)
+    syn0, syn1 = fresh()
     t0 = time.perf_counter()
-    st = oracle.train(syn0, syn1, tree, tv, p)
+    st = run(syn0, syn1, tv_all[:n])
     dt = time.perf_counter() - t0
-    return {"value": float(st[1]) / dt, "unit": "words/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {n:,} tokens ({n // w.doc_len} documents) of the same corpus, one epoch of "
-                      f"Algorithm 1 with the top-31 cache (u=10), {dt:.1f}s on one host core"}
+    print(json.dumps({"value": float(st[1]) / dt, "seconds": dt, "tokens": n,
+                      "sample": f"first {n:,} tokens ({n // w.doc_len} documents) of the same corpus, {what}, "
+                                f"{dt:.1f}s on one pinned host core"}), flush=True)
 
 
 if __name__ == "__main__":
-    main()
+    if len(sys.argv) == 3 and sys.argv[1] == "--cpu-child":
+        cpu_child(sys.argv[2])
+    else:
+        main()

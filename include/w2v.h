@@ -235,12 +235,20 @@ int w2v_last_train_launch(int32_t *workgroups_host, int32_t *wavefronts_host);
 int w2v_last_train_resources(int32_t *lds_bytes_host, int32_t *vgprs_host, int32_t *waves_per_simd_host);
 
 /* ------------------------------------------------------------------------
- * Hierarchical-softmax log-likelihood (evaluation): over the (centre,
- * context) pairs that the sampler draws from tokens with p's seed, epoch,
- * window and sample settings, sum_ll = sum of log P(v | syn0[w]) with
- * P(v|x) = prod_j sigmoid((1 - 2 t_j) x . syn1[n_j]) over v's path.
- * Dot products in fp32, logarithms and sums in fp64, summed in a fixed order
- * (deterministic). Read-only on the model. Synchronises the stream.
+ * Hierarchical-softmax log-likelihood (evaluation, §2's objective): over the
+ * (centre, context) pairs that the sampler draws from tokens with p's seed,
+ * epoch, window and sample settings, sum_ll = sum of log P(v | syn0[w]) with
+ * P(v|x) = prod_j sigmoid((1 - 2 t_j) x . syn1[n_j]) over v's path, and
+ * n_pairs = the number of pairs (p->arch 0 or 2).
+ * p->arch 1 (CBOW): the same softmax with CBOW's input, one term per sampled
+ * centre v that has at least one window word: sum_ll = sum of log P(v | h),
+ * h = the mean of the window words' syn0 rows; n_pairs = the number of such
+ * centres. n_nodes (may be NULL): the path nodes the terms visit.
+ * Skip-gram: dot products in fp32; CBOW: h and its dot products in fp64;
+ * logarithms and sums in fp64, summed in a fixed order (deterministic).
+ * Read-only on the model. Synchronises the stream. Errors: W2V_E_ARG for a
+ * bad model, params (arch outside 0..2) or NULL required pointer,
+ * W2V_E_WORKSPACE for a short workspace, W2V_E_DEVICE for a HIP failure.
  * ---------------------------------------------------------------------- */
 size_t w2v_hs_loglik_workspace_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p);
 int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,
@@ -334,23 +342,6 @@ int w2v_sample_negatives(const int32_t *tokens, int64_t n_tokens, int32_t V, con
                          int64_t train_words, const w2v_params *p, const int32_t *noise_table, int32_t log2_size,
                          int32_t *negatives, int64_t negatives_cap, int64_t *n_kept_host, uint64_t *checksum_host,
                          void *workspace, size_t workspace_bytes, void *hip_stream);
-
-/* ------------------------------------------------------------------------
- * Measurement utility (not part of the method): the practical memory ceiling
- * of the training kernel's access pattern. Wavefronts (12 per workgroup, four
- * rows in flight each) visit rows of matrix (float[rows][row_stride], device
- * memory, 16-byte aligned) picked by a 32-bit hash, iters times four rows
- * each, and read the first cols floats (mode 0) or read them, add 1 and write
- * them back (mode 1, the matrix is modified). Modes 2 and 3 visit rows
- * 0, 1, 2, ... instead, each at most once (wavefront w, round i: rows
- * 4 (w iters + i) .. +3), reading (2) or writing (3, the matrix is modified)
- * the first cols floats: dispatches of known byte counts. ms_host: kernel time
- * from HIP events on the stream. Synchronises the stream. Errors: W2V_E_ARG
- * for NULL pointers, rows < 1, cols < 1 or > min(row_stride, 1024), mode
- * not in 0..3, workgroups or iters < 1.
- * ---------------------------------------------------------------------- */
-int w2v_probe_rows(float *matrix, int64_t rows, int32_t cols, int32_t row_stride, int32_t mode, int32_t workgroups,
-                   int32_t iters, float *ms_host, void *hip_stream);
 
 #ifdef __cplusplus
 }

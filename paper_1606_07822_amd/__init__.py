@@ -114,8 +114,6 @@ def lib() -> ctypes.CDLL:
         L.w2v_sample_negatives.restype = ctypes.c_int
         L.w2v_sample_negatives.argtypes = [P, I64, I32, P, I64, ctypes.POINTER(CParams), P, I32, P, I64, P, P, P,
                                            ctypes.c_size_t, P]
-        L.w2v_probe_rows.restype = ctypes.c_int
-        L.w2v_probe_rows.argtypes = [P, I64, I32, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_float), P]
         _LIB = L
     return _LIB
 
@@ -365,7 +363,12 @@ def last_train_resources() -> dict:
 
 
 def hs_loglik(model: Model, tokens: torch.Tensor, p: Params):
-    """(sum of log P(v|w) over the sampler's pairs, n_pairs, n_nodes). Synchronises."""
+    """(sum of the held-out objective, n_terms, n_nodes). Synchronises.
+
+    p.arch 0/2: log P(v|w) summed over the sampler's pairs; p.arch 1 (CBOW):
+    log P(v|h) summed over the sampled centres with a window, h = the mean of
+    the window words' vectors.
+    """
     dev = tokens.device
     cm, cp = model.c(), p.c()
     ws = _workspace(lib().w2v_hs_loglik_workspace_bytes(ctypes.byref(cm), tokens.numel(), ctypes.byref(cp)), dev)
@@ -427,16 +430,6 @@ def kernel_source_hash() -> str:
         with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
-
-
-def probe_rows(matrix: torch.Tensor, cols: int, mode: int, workgroups: int = 256, iters: int = 1000) -> float:
-    """Kernel milliseconds of w2v_probe_rows over a float32 [rows, row_stride] GPU matrix."""
-    if matrix.dim() != 2:
-        raise ValueError("matrix must be 2-D")
-    ms = ctypes.c_float(0.0)
-    _check(lib().w2v_probe_rows(_dev_ptr(matrix, torch.float32, "matrix"), matrix.shape[0], cols, matrix.shape[1],
-                                mode, workgroups, iters, ctypes.byref(ms), _stream(matrix.device)))
-    return ms.value
 
 
 # ---------------------------------------------------------- negative sampling

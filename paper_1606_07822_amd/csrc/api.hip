@@ -30,8 +30,6 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
 size_t sync_extra_bytes(int32_t V, int32_t dim, int64_t n_docs);
 int run_train_sync(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int64_t n_tokens, Carve &c,
                    const float *alpha_tab, int64_t blk0, unsigned long long *tstats, hipStream_t s);
-int run_probe_rows(float *matrix, int64_t rows, int32_t cols, int32_t row_stride, int32_t mode, int32_t workgroups,
-                   int32_t iters, float *ms_host, hipStream_t s);
 size_t noise_workspace_bytes(int32_t V);
 int run_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, int32_t *table, int64_t *total_host,
                     void *workspace, hipStream_t s);
@@ -422,6 +420,8 @@ int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, c
     g_err.clear();
     if (int rc = check_model(m, true)) return rc;
     if (int rc = check_params(p, false)) return rc;
+    if (p->arch < 0 || p->arch > 2)
+        return fail(W2V_E_ARG, "arch must be 0 or 2 (pairs' objective) or 1 (CBOW's objective)");
     if (n_tokens < 0 || (n_tokens > 0 && !tokens)) return fail(W2V_E_ARG, "bad tokens / n_tokens");
     if (!sum_ll_host || !n_pairs_host) return fail(W2V_E_ARG, "a required pointer is NULL");
     if (int rc = check_ws(workspace, workspace_bytes, w2v_hs_loglik_workspace_bytes(m, n_tokens, p))) return rc;
@@ -558,17 +558,6 @@ int w2v_keep_thresholds(const int64_t *vocab_counts, int32_t V, double sample, i
     if (V < 1 || !vocab_counts || !thr) return fail(W2V_E_ARG, "bad arguments");
     if (!(sample >= 0.0) || sample >= 1.0) return fail(W2V_E_ARG, "sample must be in [0, 1)");
     return launch_thresholds(vocab_counts, V, sample, train_words, thr, as_stream(hip_stream));
-}
-
-int w2v_probe_rows(float *matrix, int64_t rows, int32_t cols, int32_t row_stride, int32_t mode, int32_t workgroups,
-                   int32_t iters, float *ms_host, void *hip_stream) {
-    g_err.clear();
-    if (!matrix || !ms_host) return fail(W2V_E_ARG, "matrix/ms_host is NULL");
-    if (rows < 1 || cols < 1 || row_stride < cols || cols > 1024)
-        return fail(W2V_E_ARG, "need rows >= 1 and 1 <= cols <= min(row_stride, 1024)");
-    if (mode < 0 || mode > 3) return fail(W2V_E_ARG, "mode must be in 0..3");
-    if (workgroups < 1 || iters < 1) return fail(W2V_E_ARG, "workgroups and iters must be >= 1");
-    return run_probe_rows(matrix, rows, cols, row_stride, mode, workgroups, iters, ms_host, as_stream(hip_stream));
 }
 
 }  // extern "C"

@@ -9,6 +9,9 @@
 // Log-likelihood: sum over the sampler's pairs (v, w) of
 // log P(v | syn0[w]) = sum_j log sigmoid((1 - 2 t_j) syn0[w] . syn1[n_j]);
 // dot products in fp32, logarithms and all sums in fp64, in a fixed order.
+// CBOW's objective: the same hierarchical softmax (§2) with the mean h of the
+// window words' vectors as input, one term log P(v | h) per centre that has a
+// window; h and its dot products in fp64.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -290,6 +293,7 @@ struct LLArgs {
     int32_t doc_len;
     double *unit_ll;
     int64_t *unit_nodes;
+    int64_t *unit_terms;    // CBOW: centres with a window, per unit
 };
 
 // One wavefront per work unit (a fixed assignment, so the sums are the same from run to run).
@@ -379,31 +383,101 @@ __global__ __launch_bounds__(256) void k_loglik(LLArgs a) {
     }
 }
 
-// fixed-order sum of the work units' partials
+// CBOW: one wavefront per work unit; per centre with a window, h = (sum of the window rows in
+// ascending window order, fp64) / P, then one walk of the centre's path with fp64 dot products
+// (lane n keeps the dot product of path node n and takes its log-sigmoid).
+template <int NE>
+__global__ __launch_bounds__(256) void k_loglik_cbow(LLArgs a) {
+    const int lane = lane_id();
+    const int64_t wave0 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * blockDim.x / kWave;
+    for (int64_t u = wave0; u < a.n_units; u += nwaves) {
+        const int64_t d = u / a.segs_per_doc;
+        const int nk = a.doc_kept[d];
+        const int j0 = static_cast<int>(u - d * a.segs_per_doc) * kSegLen;
+        const int j1 = min(nk, j0 + kSegLen);
+        const int64_t base = d * a.doc_len;
+        double acc = 0.0;
+        int64_t nodes = 0, terms = 0;
+        for (int j = j0; j < j1; ++j) {
+            const int v = a.kept_vid[base + j];
+            const int eff = static_cast<int>(a.kept_meta[base + j] >> 16);
+            const int clo = max(0, j - eff), chi = min(nk - 1, j + eff);
+            const int P = chi - clo;
+            if (P == 0) continue;
+            const int len = a.codelen[v];
+            const uint64_t code = a.code[v];
+            const int my_pt = (lane < len) ? a.points[a.point_off[v] + lane] : 0;
+            const int cq = clo + lane + ((clo + lane >= j) ? 1 : 0);
+            const int my_w = (lane < P) ? a.kept_vid[base + cq] : 0;
+            double h[NE];
+#pragma unroll
+            for (int i = 0; i < NE; ++i) h[i] = 0.0;
+            for (int q = 0; q < P; ++q) {
+                float x[NE];
+                buf_load_row<NE>(x, row_rsrc(const_cast<float *>(a.syn0), __builtin_amdgcn_readlane(my_w, q),
+                                             a.stride, a.dim * 4), lane);
+#pragma unroll
+                for (int i = 0; i < NE; ++i) h[i] += static_cast<double>(x[i]);
+            }
+#pragma unroll
+            for (int i = 0; i < NE; ++i) h[i] = h[i] / static_cast<double>(P);
+            double mine = 0.0;
+            for (int c = 0; c < len; ++c) {
+                float y[NE];
+                buf_load_row<NE>(y, row_rsrc(const_cast<float *>(a.syn1), __builtin_amdgcn_readlane(my_pt, c),
+                                             a.stride, a.dim * 4), lane);
+                double z = 0.0;
+#pragma unroll
+                for (int i = 0; i < NE; ++i) z += h[i] * static_cast<double>(y[i]);
+                z = wave_sum(z);
+                mine = (lane == c) ? z : mine;
+            }
+            const double sign = ((code >> min(lane, 63)) & 1ull) ? -1.0 : 1.0;
+            if (lane < len) acc += log_sigmoid(sign * mine);
+            nodes += len;
+            terms += 1;
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) {
+            a.unit_ll[u] = acc;
+            a.unit_nodes[u] = nodes;
+            a.unit_terms[u] = terms;
+        }
+    }
+}
+
+// fixed-order sum of the work units' partials (terms: optional)
 __global__ __launch_bounds__(1024) void k_sum_docs(const double *__restrict__ ll, const int64_t *__restrict__ nodes,
-                                                   int64_t n, double *__restrict__ out_ll,
-                                                   int64_t *__restrict__ out_nodes) {
+                                                   const int64_t *__restrict__ terms, int64_t n,
+                                                   double *__restrict__ out_ll, int64_t *__restrict__ out_nodes,
+                                                   int64_t *__restrict__ out_terms) {
     __shared__ double sl[1024];
     __shared__ int64_t sn[1024];
+    __shared__ int64_t st_[1024];
     double a = 0.0;
-    int64_t b = 0;
+    int64_t b = 0, t = 0;
     for (int64_t i = threadIdx.x; i < n; i += 1024) {
         a += ll[i];
         b += nodes[i];
+        if (terms) t += terms[i];
     }
     sl[threadIdx.x] = a;
     sn[threadIdx.x] = b;
+    st_[threadIdx.x] = t;
     __syncthreads();
     for (int st = 512; st > 0; st >>= 1) {
         if (threadIdx.x < st) {
             sl[threadIdx.x] += sl[threadIdx.x + st];
             sn[threadIdx.x] += sn[threadIdx.x + st];
+            st_[threadIdx.x] += st_[threadIdx.x + st];
         }
         __syncthreads();
     }
     if (threadIdx.x == 0) {
         *out_ll = sl[0];
         *out_nodes = sn[0];
+        *out_terms = st_[0];
     }
 }
 
@@ -419,6 +493,16 @@ LLFn pick_ll(int dim) {
     return k_loglik<16, 2>;
 }
 
+LLFn pick_ll_cbow(int dim) {
+    const int ne = (dim + kWave - 1) / kWave;
+    if (ne <= 1) return k_loglik_cbow<1>;
+    if (ne <= 2) return k_loglik_cbow<2>;
+    if (ne <= 4) return k_loglik_cbow<4>;
+    if (ne <= 5) return k_loglik_cbow<5>;
+    if (ne <= 8) return k_loglik_cbow<8>;
+    return k_loglik_cbow<16>;
+}
+
 }  // namespace
 
 int64_t loglik_units(int64_t n_tokens, int32_t doc_len) {
@@ -429,8 +513,9 @@ size_t loglik_extra_bytes(int64_t n_units) {
     Carve c;
     c.take<double>(static_cast<size_t>(n_units));
     c.take<int64_t>(static_cast<size_t>(n_units));
+    c.take<int64_t>(static_cast<size_t>(n_units));
     c.take<double>(1);
-    c.take<int64_t>(1);
+    c.take<int64_t>(2);
     return c.used();
 }
 
@@ -454,27 +539,31 @@ int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int
     a.doc_len = p->doc_len;
     a.unit_ll = c.take<double>(static_cast<size_t>(n_units));
     a.unit_nodes = c.take<int64_t>(static_cast<size_t>(n_units));
+    a.unit_terms = c.take<int64_t>(static_cast<size_t>(n_units));
     double *out = c.take<double>(1);
-    int64_t *out_nodes = c.take<int64_t>(1);
+    int64_t *out_nt = c.take<int64_t>(2);   // nodes, terms
+    const bool cbow = p->arch == 1;
     if (a.n_units > 0) {
         const unsigned grid =
             static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_units, 4), 16LL * device_cu_count()));
-        hipLaunchKernelGGL(pick_ll(m->dim), dim3(grid), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(cbow ? pick_ll_cbow(m->dim) : pick_ll(m->dim), dim3(grid), dim3(256), 0, s, a);
         W2V_LAUNCH_CHECK("k_loglik");
-        k_sum_docs<<<1, 1024, 0, s>>>(a.unit_ll, a.unit_nodes, a.n_units, out, out_nodes);
+        k_sum_docs<<<1, 1024, 0, s>>>(a.unit_ll, a.unit_nodes, cbow ? a.unit_terms : nullptr, a.n_units, out,
+                                      out_nt, out_nt + 1);
         W2V_LAUNCH_CHECK("k_sum_docs");
     }
     double hll = 0.0;
-    int64_t nn = 0;
+    int64_t nt[2] = {0, 0};
     int64_t tot[4] = {0, 0, 0, 0};
     if (a.n_units > 0) {
         W2V_HIP(hipMemcpyAsync(&hll, out, sizeof(hll), hipMemcpyDeviceToHost, s));
-        W2V_HIP(hipMemcpyAsync(&nn, out_nodes, sizeof(nn), hipMemcpyDeviceToHost, s));
+        W2V_HIP(hipMemcpyAsync(nt, out_nt, sizeof(nt), hipMemcpyDeviceToHost, s));
     }
     W2V_HIP(hipMemcpyAsync(tot, b.totals, sizeof(tot), hipMemcpyDeviceToHost, s));
     W2V_HIP(hipStreamSynchronize(s));
+    const int64_t nn = nt[0];
     *sum_ll_host = hll;
-    *n_pairs_host = tot[3];
+    *n_pairs_host = cbow ? nt[1] : tot[3];
     if (n_nodes_host) *n_nodes_host = nn;
     return W2V_OK;
 }

@@ -52,3 +52,15 @@ def row_rel_err(a: np.ndarray, b: np.ndarray) -> float:
     s = np.abs(b.astype(np.float64)).max(axis=1)
     r = np.where(s > 0, d / np.where(s > 0, s, 1), d)
     return float(r.max()) if r.size else 0.0
+
+
+def ll_gate(gpu_ll: float, oracle_ll: float, init_ll: float, min_gain_frac: float | None = None) -> float:
+    """The asynchronous-mode quality gate: the GPU's held-out mean log-likelihood within 1 % of the
+    sequential oracle's, and (optionally) at least min_gain_frac of the oracle's gain over the untrained
+    model, (init - gpu) / (init - oracle). Returns the gain fraction."""
+    frac = (gpu_ll - init_ll) / (oracle_ll - init_ll)
+    log(f"  gpu {gpu_ll:.6f} oracle {oracle_ll:.6f} init {init_ll:.6f} gain fraction {frac:.4f}")
+    assert abs(gpu_ll - oracle_ll) <= 0.01 * abs(oracle_ll), (gpu_ll, oracle_ll)
+    if min_gain_frac is not None:
+        assert frac >= min_gain_frac, (frac, min_gain_frac)
+    return frac

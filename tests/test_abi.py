@@ -157,13 +157,20 @@ def test_binding_refuses_host_tensors(w2v):
     ((0x1000, 10, 4, 4, 4, 1, 1), "mode"),
     ((0x1000, 10, 4, 4, 0, 0, 1), "workgroups"),
 ])
-def test_probe_argument_errors(w2v, args, msg):
+def test_probe_argument_errors(args, msg):
+    import bench_probe
     ms = ctypes.c_float(0.0)
     m, rows, cols, stride, mode, wg, it = args
-    rc = w2v.lib().w2v_probe_rows(ctypes.c_void_p(m) if m else None, rows, cols, stride, mode, wg, it,
-                                  ctypes.byref(ms), None)
-    assert rc == w2v.W2V_E_ARG
-    assert msg in w2v.last_error()
+    rc = bench_probe.lib().w2v_probe_rows(ctypes.c_void_p(m) if m else None, rows, cols, stride, mode, wg, it,
+                                          ctypes.byref(ms), None)
+    assert rc == -1
+    assert msg in bench_probe.last_error()
+
+
+def test_probe_is_not_in_the_library(w2v):
+    import bench_probe
+    assert not hasattr(w2v.lib(), "w2v_probe_rows")
+    assert hasattr(bench_probe.lib(), "w2v_probe_rows")
 
 
 def test_struct_offset_of_negative(w2v):
