@@ -256,6 +256,26 @@ int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, c
                   size_t workspace_bytes, void *hip_stream);
 
 /* ------------------------------------------------------------------------
+ * w2v_hs_loglik on the library's own scratch memory, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, results and errors as
+ * w2v_hs_loglik without the workspace: the workspace is a static device
+ * array of w2v_noalloc_scratch_bytes() bytes (64 MiB) that every GPU the
+ * library runs on holds until the process ends. The call itself allocates
+ * nothing; its first call on a device looks up that device's copy of the
+ * array. Evaluations whose w2v_hs_loglik_workspace_bytes exceed the scratch
+ * return W2V_E_RANGE before anything is launched (8 bytes per token plus
+ * 8 bytes per vocabulary word and some per-document counts: e.g. V = 1M
+ * with up to about 6M tokens). Every call on a device shares that device's
+ * scratch, which keeps the last call's contents: calls that overlap on one
+ * device (other streams or threads) race on it and must not be issued
+ * concurrently. Synchronises the stream.
+ * ---------------------------------------------------------------------- */
+size_t w2v_noalloc_scratch_bytes(void);
+int w2v_hs_loglik_noalloc(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,
+                          double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, void *hip_stream);
+
+/* ------------------------------------------------------------------------
  * Negative sampling: the alternative objective to the hierarchical softmax
  * that §2 names, trained in the mini-batch form of Ji et al. that the opening
  * of §3.2 describes (every window word of a centre trains against the same

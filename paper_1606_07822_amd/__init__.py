@@ -109,6 +109,10 @@ def lib() -> ctypes.CDLL:
         L.w2v_ns_objective.restype = ctypes.c_int
         L.w2v_ns_objective.argtypes = [ctypes.POINTER(CModel), P, I32, P, I64, ctypes.POINTER(CParams), P, P, P, P,
                                        ctypes.c_size_t, P]
+        L.w2v_noalloc_scratch_bytes.restype = ctypes.c_size_t
+        L.w2v_noalloc_scratch_bytes.argtypes = []
+        L.w2v_hs_loglik_noalloc.restype = ctypes.c_int
+        L.w2v_hs_loglik_noalloc.argtypes = [ctypes.POINTER(CModel), P, I64, ctypes.POINTER(CParams), P, P, P, P]
         L.w2v_sample_negatives_workspace_bytes.restype = ctypes.c_size_t
         L.w2v_sample_negatives_workspace_bytes.argtypes = [I32, I64, ctypes.POINTER(CParams)]
         L.w2v_sample_negatives.restype = ctypes.c_int
@@ -378,6 +382,19 @@ def hs_loglik(model: Model, tokens: torch.Tensor, p: Params):
     _check(lib().w2v_hs_loglik(ctypes.byref(cm), _dev_ptr(tokens, torch.int32, "tokens"), tokens.numel(),
                                ctypes.byref(cp), ctypes.byref(s), ctypes.byref(npairs), ctypes.byref(nn),
                                ws.data_ptr(), ws.numel(), _stream(dev)))
+    return s.value, npairs.value, nn.value
+
+
+def hs_loglik_noalloc(model: Model, tokens: torch.Tensor, p: Params):
+    """hs_loglik on the library's static scratch (no workspace is allocated). Synchronises."""
+    dev = tokens.device
+    cm, cp = model.c(), p.c()
+    s = ctypes.c_double(0)
+    npairs = ctypes.c_int64(0)
+    nn = ctypes.c_int64(0)
+    _check(lib().w2v_hs_loglik_noalloc(ctypes.byref(cm), _dev_ptr(tokens, torch.int32, "tokens"), tokens.numel(),
+                                       ctypes.byref(cp), ctypes.byref(s), ctypes.byref(npairs), ctypes.byref(nn),
+                                       _stream(dev)))
     return s.value, npairs.value, nn.value
 
 

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libw2v.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "vocab.hip", "huffman.hip", "sampling.hip", "train.hip", "sync_loglik.hip", "negative.hip"]
+SOURCES = ["api.hip", "vocab.hip", "huffman.hip", "sampling.hip", "train.hip", "sync_loglik.hip", "negative.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "--offload-arch=gfx950", "-fPIC", "-std=c++17", "-munsafe-fp-atomics",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -239,6 +239,29 @@ size_t train_bytes(const w2v_model *m, int64_t n_tokens, const w2v_params *p) {
 
 }  // namespace
 
+namespace w2v {
+
+int check_loglik_args(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,
+                      const double *sum_ll_host, const int64_t *n_pairs_host) {
+    if (int rc = check_model(m, true)) return rc;
+    if (int rc = check_params(p, false)) return rc;
+    if (p->arch < 0 || p->arch > 2)
+        return fail(W2V_E_ARG, "arch must be 0 or 2 (pairs' objective) or 1 (CBOW's objective)");
+    if (n_tokens < 0 || (n_tokens > 0 && !tokens)) return fail(W2V_E_ARG, "bad tokens / n_tokens");
+    if (!sum_ll_host || !n_pairs_host) return fail(W2V_E_ARG, "a required pointer is NULL");
+    return W2V_OK;
+}
+
+int loglik_run(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p, double *sum_ll_host,
+               int64_t *n_pairs_host, int64_t *n_nodes_host, void *workspace, hipStream_t s) {
+    Carve c(workspace);
+    SampleBufs b = sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
+    if (int rc = launch_sampling(tokens, n_tokens, m->V, m->vocab_counts, m->train_words, p, b, nullptr, s)) return rc;
+    return run_loglik(m, p, b, n_tokens, c, sum_ll_host, n_pairs_host, n_nodes_host, s);
+}
+
+}  // namespace w2v
+
 extern "C" {
 
 const char *w2v_last_error(void) { return g_err.c_str(); }
@@ -418,18 +441,10 @@ int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, c
                   double *sum_ll_host, int64_t *n_pairs_host, int64_t *n_nodes_host, void *workspace,
                   size_t workspace_bytes, void *hip_stream) {
     g_err.clear();
-    if (int rc = check_model(m, true)) return rc;
-    if (int rc = check_params(p, false)) return rc;
-    if (p->arch < 0 || p->arch > 2)
-        return fail(W2V_E_ARG, "arch must be 0 or 2 (pairs' objective) or 1 (CBOW's objective)");
-    if (n_tokens < 0 || (n_tokens > 0 && !tokens)) return fail(W2V_E_ARG, "bad tokens / n_tokens");
-    if (!sum_ll_host || !n_pairs_host) return fail(W2V_E_ARG, "a required pointer is NULL");
+    if (int rc = check_loglik_args(m, tokens, n_tokens, p, sum_ll_host, n_pairs_host)) return rc;
     if (int rc = check_ws(workspace, workspace_bytes, w2v_hs_loglik_workspace_bytes(m, n_tokens, p))) return rc;
-    hipStream_t s = as_stream(hip_stream);
-    Carve c(workspace);
-    SampleBufs b = sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
-    if (int rc = launch_sampling(tokens, n_tokens, m->V, m->vocab_counts, m->train_words, p, b, nullptr, s)) return rc;
-    return run_loglik(m, p, b, n_tokens, c, sum_ll_host, n_pairs_host, n_nodes_host, s);
+    return loglik_run(m, tokens, n_tokens, p, sum_ll_host, n_pairs_host, n_nodes_host, workspace,
+                      as_stream(hip_stream));
 }
 
 size_t w2v_noise_table_workspace_bytes(int32_t V) { return V < 1 ? 0 : noise_workspace_bytes(V); }

@@ -268,4 +268,11 @@ struct TrainArgs {
     int32_t egrad_slots;
 };
 
+// The log-likelihood call's argument checks and body (workspace of w2v_hs_loglik_workspace_bytes bytes),
+// shared by w2v_hs_loglik and its variant on the library's static scratch.
+int check_loglik_args(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p,
+                      const double *sum_ll_host, const int64_t *n_pairs_host);
+int loglik_run(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, const w2v_params *p, double *sum_ll_host,
+               int64_t *n_pairs_host, int64_t *n_nodes_host, void *workspace, hipStream_t s);
+
 }  // namespace w2v

@@ -279,3 +279,21 @@ def test_train_word_span_argument_errors(w2v):
     assert "NULL" in w2v.last_error()
     assert L.w2v_train_word_span(ctypes.byref(_model(w2v)), ctypes.byref(_params(w2v, write_policy=8))) == -1
     assert "needs bit 1" in w2v.last_error()
+
+
+def test_noalloc_loglik_rejects_what_the_scratch_cannot_hold(w2v):
+    """Checked on the host before any device call: a model of V = 1M and 10M tokens needs more
+    workspace than the static scratch."""
+    fake = ctypes.c_void_p(0x1000)
+    cm = w2v.CModel(syn0=fake, syn1=fake, V=1_000_000, dim=300, row_stride=320, vocab_counts=fake, train_words=10**9,
+                    codelen=fake, code=fake, point_off=fake, points=fake)
+    p = w2v.Params(window=5).c()
+    need = w2v.lib().w2v_hs_loglik_workspace_bytes(ctypes.byref(cm), 10_000_000, ctypes.byref(p))
+    assert need > w2v.lib().w2v_noalloc_scratch_bytes() == 64 << 20
+    s, n, nn = ctypes.c_double(0), ctypes.c_int64(0), ctypes.c_int64(0)
+    rc = w2v.lib().w2v_hs_loglik_noalloc(ctypes.byref(cm), fake, 10_000_000, ctypes.byref(p), ctypes.byref(s),
+                                         ctypes.byref(n), ctypes.byref(nn), None)
+    assert rc == w2v.W2V_E_RANGE and "scratch" in w2v.last_error()
+    rc = w2v.lib().w2v_hs_loglik_noalloc(ctypes.byref(cm), fake, 10, ctypes.byref(p), None, ctypes.byref(n),
+                                         ctypes.byref(nn), None)
+    assert rc == w2v.W2V_E_ARG
