@@ -11,6 +11,10 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
     config.addinivalue_line("markers", "slow: takes more than a few seconds on the CPU")
+    # W2V_TEST_LIB: run the tests against another build of libw2v (the sanitizer build of the host code)
+    if os.environ.get("W2V_TEST_LIB"):
+        import paper_1606_07822_amd
+        paper_1606_07822_amd.LIB_PATH = os.environ["W2V_TEST_LIB"]
 
 
 @pytest.fixture(scope="session", autouse=True)
