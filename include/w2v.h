@@ -161,7 +161,11 @@ typedef struct {
                                 1 = delta-only: it holds just its change since the last write-back, reads a
                                 cached row as the HBM row plus that change and adds its updates to the change
                                 with LDS atomics (write_policy bit 2 does not apply); half the LDS per row */
-    int32_t reserved2[3];
+    int32_t span_refresh;    /* with write_policy bit 3 in effect: the words of vocabulary index below this
+                                (the most frequent) are written back, if changed, and read again after every
+                                centre while they stay in the span, so that other wavefronts' updates to them
+                                are lost for one centre at most, as without bit 3; 0 = off; >= 0 */
+    int32_t reserved2[2];
 } w2v_params;
 
 /* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,

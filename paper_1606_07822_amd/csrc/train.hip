@@ -465,7 +465,8 @@ __device__ __forceinline__ void walk_path(const TrainArgs &a, float *val, const 
 // H-(j-lo) .. H+(hi-j)-1, in window order. A row is loaded when its position comes within H of
 // the centre and stored when it leaves the span or becomes the centre, so each word row is read
 // and written about twice per centre instead of once per pair. Slots holding the same word are
-// kept equal: a change made to one is added to the others, and a word entering the span is copied
+// kept equal (up to the order in which they add each other's changes): a change made to one is added to
+// the others, and a word entering the span is copied
 // from a slot that holds it rather than read from memory.
 template <int PG>
 __device__ __forceinline__ int span_pairs(int sid, int lane) {
@@ -584,6 +585,20 @@ __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs 
                                            int &pairs, int v, int w_edge, int lane) {
     constexpr int H = PG / 2;
     constexpr uint32_t low = (1u << (H - 1)) - 1u;
+    // frequent words (index below span_refresh) that stay in the span are written back here and read
+    // again after the shift, which bounds how long other wavefronts' updates to them can be overwritten
+    const bool refresh = a.span_refresh > 0;
+    if (refresh) {
+#pragma unroll
+        for (int q = 1; q < PG; ++q) {
+            if (q == H) continue;
+            const int w = __builtin_amdgcn_readlane(sid, q);
+            if (w >= 0 && w < a.span_refresh && ((dirty >> q) & 1u)) {
+                span_store<NE, PG>(xw, q, a, sid, lane);
+                dirty &= ~(1u << q);
+            }
+        }
+    }
     if (dirty & 1u) span_store<NE, PG>(xw, 0, a, sid, lane);
     if ((dirty >> H) & 1u) span_store<NE, PG>(xw, H, a, sid, lane);
     if (pairs > 0) {   // equal pairs that slots 0 and H leave behind
@@ -603,6 +618,14 @@ __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs 
     const int src = (lane < H - 1 || (lane >= H && lane < PG - 1)) ? lane + 1 : lane;
     sid = __shfl(sid, src, kWave);
     sid = lane == H - 1 ? v : (lane == PG - 1 ? w_edge : sid);
+    if (refresh) {
+#pragma unroll
+        for (int q = 0; q < PG - 1; ++q) {
+            if (q == H - 1) continue;
+            const int w = __builtin_amdgcn_readlane(sid, q);
+            if (w >= 0 && w < a.span_refresh) span_load<NE, PG>(xw, q, a, sid, lane);
+        }
+    }
     dirty |= span_enter<NE, PG, H - 1>(xw, a, sid, dirty, pairs, lane) << (H - 1);
     dirty |= span_enter<NE, PG, PG - 1>(xw, a, sid, dirty, pairs, lane) << (PG - 1);
 }
@@ -729,9 +752,11 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                         n_nodes += len;
                     } else if constexpr (SLIDE) {
                         const int p0 = H - (j - lo), p1 = H + (hi - j);
+                        // only the active slots' gradients are accumulated, read and applied
                         float e[PG][NE];
 #pragma unroll
-                        for (int q = 0; q < PG; ++q) zero_row<NE>(e[q]);
+                        for (int q = 0; q < PG; ++q)
+                            if (q >= p0 && q < p1) zero_row<NE>(e[q]);
                         walk_path<NE, PG, PF>(a, val, xw, e, p0, p1, my_pt, len, code, alpha, lane);
                         span_apply<NE, PG>(xw, e, p0, p1, sid, pairs > 0, dirty, lane);
                         n_nodes += static_cast<uint64_t>(P) * len;

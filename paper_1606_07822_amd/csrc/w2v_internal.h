@@ -262,6 +262,7 @@ struct TrainArgs {
     int32_t stores_only;     // train_stores_only(): every inner-node row is written back by a store
     float flush_scale;       // fraction of the cached rows' change written back (1 = all of it)
     int32_t cache_delta;     // delta-only cache: LDS holds the workgroup's change of each cached row only
+    int32_t span_refresh;    // word-row span: words below this index are written back and re-read every centre
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, node updates
     float *egrad;            // per wavefront egrad_slots rows of row_stride floats (parked gradients), or null

@@ -372,6 +372,39 @@ def test_single_worker_word_rows_kept_across_centres(w2v, arch, name, sample, k,
     np.testing.assert_array_equal(g0[untouched], syn0[untouched])
 
 
+# span_refresh writes the span's frequent words back and reads them again after every centre. One wavefront
+# reads what it wrote, so it still reproduces the centre-major oracle; the result can differ from the run
+# without it in rounding only (slots holding the same word take each other's changes in different orders, and
+# the refresh decides which slot's rounding is kept).
+@pytest.mark.parametrize("arch,name,sample,dim,refresh", [
+    (0, "tiny_sg_v1k_d50", 0.0, 300, 10), (0, "tiny_sg_v1k_d50", 0.0, 300, 10**6), (0, "sg_v30k_d100", 1e-3, 200, 500),
+    (1, "tiny_sg_v1k_d50", 0.0, 300, 50),
+])
+def test_span_refresh_single_worker_matches_oracle(w2v, arch, name, sample, dim, refresh):
+    log(f"span refresh arch={arch} {name} dim={dim} refresh={refresh}")
+    s = oracle_side(name)
+    voc, tree = gpu_side(w2v, s)
+    tv = s.tv[:3000]
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
+    alpha0 = 0.05 if arch else 0.025
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, dim, window=5, sample=sample, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, cache_k=31, flush_every=10, order=1, arch=arch, alpha0=alpha0)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    out = []
+    for r in (0, refresh):
+        model = w2v.make_model(syn0, syn1, voc, tree)
+        p = w2v.Params(window=5, sample=sample, corpus_tokens=s.tv.size, cache_k=31, flush_every=10, workers=1,
+                       write_policy=15, arch=arch, alpha0=alpha0, span_refresh=r)
+        assert w2v.train_word_span(model, p) == 5
+        st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+        assert list(st) == list(ost)
+        g0, g1 = (t.cpu().numpy() for t in model.vectors())
+        assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+        out.append((g0, g1))
+    assert row_rel_err(out[1][0], out[0][0]) <= 1e-5
+
+
 def async_ll(w2v, s, held, **kw):
     voc, tree = gpu_side(w2v, s)
     syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim)
