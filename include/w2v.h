@@ -149,8 +149,11 @@ typedef struct {
                                 (bit 0; bit 2 when cache_k > 0; hot_k 0; cache_mode 0) and with window <= 2
                                 above 320 floats; elsewhere the bit is ignored; w2v_train_word_span reports
                                 which */
-    int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), 1 = add the
-                                change divided by the number of workgroups (their progress averaged) */
+    int32_t flush_policy;    /* cache write-back: 0 = add the change (cached - original), the write-back of
+                                §3.2 as printed (stable at a few hundred wavefronts; at full occupancy the
+                                top rows' summed stale changes diverge); 1 = add the change divided by the
+                                number of workgroups, so that their progress on the cached rows is averaged
+                                (local SGD on those rows) -- a departure from §3.2, and the default */
     int32_t hot_k;           /* with write_policy bit 0: the hot_k inner nodes created just before the cached
                                 ones (on most paths, so the most contended rows) still take atomic adds of
                                 their change; >= 0 */

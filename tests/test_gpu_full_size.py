@@ -210,4 +210,4 @@ def test_full_prefix_async_loglik_within_1pct(w2v, wp):
     held = to_dev(oracle.remap(corpus(NAME, heldout=True), ov.id_to_vocab))
     s, npairs, _ = w2v.hs_loglik(model, held, w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL))
     assert npairs == g["heldout_pairs"]
-    ll_gate(s / npairs, g["mean_ll"], g["init_mean_ll"])
+    ll_gate(s / npairs, g["mean_ll"], g["init_mean_ll"], 0.9)

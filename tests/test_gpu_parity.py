@@ -443,30 +443,31 @@ def golden(name):
     return json.load(open(path))
 
 
-# Default asynchronous mode (top-31 cache in LDS, write-back of the workgroups' averaged change every
+# Every case must also keep at least 0.9 of the oracle's gain over the untrained model (the 1 % bound alone
+# would let the 1e7-token workload lose 62 % of it). Default asynchronous mode (top-31 cache in LDS, write-back of the workgroups' averaged change every
 # 1000 centres, Hogwild row stores in HBM and in the LDS copy) at full occupancy; the same with atomic adds
 # of the change everywhere (write_policy 0) or in LDS only (1); no cache; and the cache with the paper's
 # summed write-back, which is stable only at low concurrency (256 wavefronts). CBOW's default also adds
 # the change atomically on the 1024 hot rows below the cache. write_policy 7 (word rows stored too) is
 # the benchmark's setting; cache_mode 1 the delta-only cache.
 @pytest.mark.parametrize("name,kw,min_frac", [
-    ("sg_v30k_d100", {}, None),
-    ("sg_v30k_d100", dict(write_policy=7), None),
-    ("sg_v30k_d100", dict(write_policy=0), None),
-    ("sg_v30k_d100", dict(write_policy=1), None),
-    ("sg_v30k_d100", dict(cache_k=0), None),
-    ("sg_v30k_d100", dict(workers=256, cache_k=31, flush_every=10, flush_policy=0, write_policy=0), None),
-    ("sg_v30k_d100", dict(cache_mode=1), None),
-    ("sg_v30k_d100", dict(cache_mode=1, cache_k=63, flush_every=100), None),
-    ("sg_v100k_d200", {}, None),
-    ("sg_v100k_d200", dict(write_policy=0), None),
-    ("sg_v100k_d200", dict(write_policy=1), None),
-    ("sg_v100k_d200", dict(write_policy=7), None),
-    ("sg_v100k_d200", dict(write_policy=15), None),
-    ("sg_v100k_d200", dict(cache_mode=1), None),
-    ("cbow_v100k_d300", {}, None),
-    ("cbow_v100k_d300", dict(write_policy=7), None),
-    ("cbow_v100k_d300", dict(write_policy=15), None),
+    ("sg_v30k_d100", {}, 0.9),
+    ("sg_v30k_d100", dict(write_policy=7), 0.9),
+    ("sg_v30k_d100", dict(write_policy=0), 0.9),
+    ("sg_v30k_d100", dict(write_policy=1), 0.9),
+    ("sg_v30k_d100", dict(cache_k=0), 0.9),
+    ("sg_v30k_d100", dict(workers=256, cache_k=31, flush_every=10, flush_policy=0, write_policy=0), 0.9),
+    ("sg_v30k_d100", dict(cache_mode=1), 0.9),
+    ("sg_v30k_d100", dict(cache_mode=1, cache_k=63, flush_every=100), 0.9),
+    ("sg_v100k_d200", {}, 0.9),
+    ("sg_v100k_d200", dict(write_policy=0), 0.9),
+    ("sg_v100k_d200", dict(write_policy=1), 0.9),
+    ("sg_v100k_d200", dict(write_policy=7), 0.9),
+    ("sg_v100k_d200", dict(write_policy=15), 0.9),
+    ("sg_v100k_d200", dict(cache_mode=1), 0.9),
+    ("cbow_v100k_d300", {}, 0.9),
+    ("cbow_v100k_d300", dict(write_policy=7), 0.9),
+    ("cbow_v100k_d300", dict(write_policy=15), 0.9),
 ])
 def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw, min_frac):
     log(f"async LL {name} {kw}")
@@ -575,4 +576,4 @@ def test_async_loglik_reversed_and_epochs(w2v, name, gold, arch, epochs):
     hv = to_dev(oracle.remap(held, s.voc.id_to_vocab))
     sg, npairs, _ = w2v.hs_loglik(model, hv, w2v.Params(window=s.w.window, sample=s.w.sample, seed=synth.SEED_EVAL))
     assert npairs == g["heldout_pairs"]
-    ll_gate(sg / npairs, g["mean_ll"], g["init_mean_ll"])
+    ll_gate(sg / npairs, g["mean_ll"], g["init_mean_ll"], 0.9)
