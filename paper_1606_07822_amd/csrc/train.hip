@@ -494,14 +494,21 @@ __device__ __forceinline__ void span_store(const float (&xw)[PG][NE], int q, con
 
 // Slot DST takes a new word w (sid already updated): a copy of a slot below PG - 1 other than DST
 // that holds w, else the row from memory. Returns the slot's dirty bit.
+// pre: when pre_ok, the row of w as this wavefront last held it, which memory also holds in a one-wavefront
+// run (the stashed row of the centre word, re-entering the span as slot H-1).
 template <int NE, int PG, int DST>
 __device__ __forceinline__ uint32_t span_enter(float (&xw)[PG][NE], const TrainArgs &a, int sid, uint32_t dirty,
-                                               int &pairs, int lane) {
+                                               int &pairs, int lane, const float (&pre)[NE], bool pre_ok) {
     const int w = __builtin_amdgcn_readlane(sid, DST);
     const uint64_t m = w >= 0 ? __ballot(lane < PG - 1 && lane != DST && sid == w) : 0ull;
     pairs += __popcll(m);
     if (m == 0ull) {
-        span_load<NE, PG>(xw, DST, a, sid, lane);
+        if (pre_ok) {
+#pragma unroll
+            for (int i = 0; i < NE; ++i) xw[DST][i] = pre[i];
+        } else {
+            span_load<NE, PG>(xw, DST, a, sid, lane);
+        }
         return 0u;
     }
     // the copy goes through an empty asm statement per slot, which keeps the slots' branches apart (merged,
@@ -580,11 +587,29 @@ __device__ __forceinline__ void span_apply_same(float (&xw)[PG][NE], const float
 // Move the span from centre j to centre j+1: slot 0 (position j-H) and slot H (position j+1, the
 // next centre) leave, stored if changed; the rest shift down one slot; slot H-1 takes the old centre
 // word v and slot PG-1 the word at position j+1+H (w_edge, -1 past the document's end).
+// stash (LDS, one row per wavefront, or null): slot H's row is the next centre's word, which leaves the span
+// now and comes back as slot H-1 at the next shift; its row is kept in the stash meanwhile (stash_w: the
+// word stashed, -1 for none) and taken from there instead of memory, unless another slot holds the word
+// or a slot leaving at that shift wrote it back.
 template <int NE, int PG>
 __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs &a, int &sid, uint32_t &dirty,
-                                           int &pairs, int v, int w_edge, int lane) {
+                                           int &pairs, int v, int w_edge, int lane, float *stash, int &stash_w) {
     constexpr int H = PG / 2;
     constexpr uint32_t low = (1u << (H - 1)) - 1u;
+    float back[NE];            // the current centre's row, stashed at the previous shift
+    bool back_ok = false;
+    if (stash) {
+        const int w0 = __builtin_amdgcn_readlane(sid, 0), wh = __builtin_amdgcn_readlane(sid, H);
+        back_ok = stash_w >= 0 && stash_w == v && !((dirty & 1u) && w0 == v) && !(((dirty >> H) & 1u) && wh == v) &&
+                  !(v < a.span_refresh);
+        if (back_ok) {
+#pragma unroll
+            for (int i = 0; i < NE; ++i) back[i] = stash[lane + i * kWave];
+        }
+#pragma unroll
+        for (int i = 0; i < NE; ++i) stash[lane + i * kWave] = xw[H][i];
+        stash_w = wh;
+    }
     // frequent words (index below span_refresh) that stay in the span are written back here and read
     // again after the shift, which bounds how long other wavefronts' updates to them can be overwritten
     const bool refresh = a.span_refresh > 0;
@@ -626,8 +651,8 @@ __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs 
             if (w >= 0 && w < a.span_refresh) span_load<NE, PG>(xw, q, a, sid, lane);
         }
     }
-    dirty |= span_enter<NE, PG, H - 1>(xw, a, sid, dirty, pairs, lane) << (H - 1);
-    dirty |= span_enter<NE, PG, PG - 1>(xw, a, sid, dirty, pairs, lane) << (PG - 1);
+    dirty |= span_enter<NE, PG, H - 1>(xw, a, sid, dirty, pairs, lane, back, back_ok) << (H - 1);
+    dirty |= span_enter<NE, PG, PG - 1>(xw, a, sid, dirty, pairs, lane, back, false) << (PG - 1);
 }
 
 
@@ -703,6 +728,8 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
             int sid = -1;
             uint32_t dirty = 0;
             int pairs = 0;   // slot pairs holding the same word
+            float *stash = (SLIDE && a.stash_off >= 0) ? lds + a.stash_off + wib * NE * kWave : nullptr;
+            int stash_w = -1;
             if constexpr (SLIDE) {
                 const int pos = lane < H ? j0 - H + lane : j0 + 1 + lane - H;
                 sid = (lane < PG && pos >= 0 && pos < nk) ? kv[pos] : -1;
@@ -904,7 +931,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     }
                 }
                 if constexpr (SLIDE) {
-                    if (j + 1 < j1) span_shift<NE, PG>(xw, a, sid, dirty, pairs, v, w_edge, lane);
+                    if (j + 1 < j1) span_shift<NE, PG>(xw, a, sid, dirty, pairs, v, w_edge, lane, stash, stash_w);
                 }
             }
             if constexpr (SLIDE) {
@@ -986,6 +1013,14 @@ size_t train_lds_bytes(int32_t cache_k, int32_t dim, bool delta) {
     return (delta ? 1ull : 2ull) * cache_k * v.ls(dim) * sizeof(float) + static_cast<size_t>(v.rec_bytes);
 }
 
+// Dynamic LDS of the word-row span's stash (one row per wavefront) when it fits beside the cache and the
+// centre records; 0 otherwise (the span then reads the re-entering centre word from memory).
+size_t span_stash_bytes(const Variant &v, size_t cache_lds, bool slide) {
+    if (!slide) return 0;
+    const size_t b = static_cast<size_t>(v.waves_per_block) * v.ne * kWave * sizeof(float);
+    return cache_lds + b + static_cast<size_t>(v.rec_bytes) + 1024 <= device_max_lds() ? b : 0;
+}
+
 int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int workers, int64_t n_units, int *grid,
                        int *waves, bool slide) {
     const Variant v = pick_variant(arch, dim, buf, slide);
@@ -994,7 +1029,8 @@ int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int
         *waves = workers;
         return W2V_OK;
     }
-    const size_t lds = (delta ? 1ull : 2ull) * cache_k * v.ls(dim) * sizeof(float);
+    const size_t cache_lds = (delta ? 1ull : 2ull) * cache_k * v.ls(dim) * sizeof(float);
+    const size_t lds = cache_lds + span_stash_bytes(v, cache_lds, slide);
     int per_cu = 0;
     W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(v.fn),
                                                          v.waves_per_block * kWave, lds));
@@ -1031,7 +1067,10 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
                        int64_t *stats_out, const int64_t *totals) {
     const bool slide = train_slide(arch, a.dim, a.stores_only != 0, a.write_policy, window);
     const Variant v = pick_variant(arch, a.dim, a.stores_only != 0, slide);
-    const size_t lds = (a.cache_delta ? 1ull : 2ull) * a.cache_k * v.ls(a.dim) * sizeof(float);
+    const size_t cache_lds = (a.cache_delta ? 1ull : 2ull) * a.cache_k * v.ls(a.dim) * sizeof(float);
+    const size_t stash = span_stash_bytes(v, cache_lds, slide);
+    a.stash_off = stash ? static_cast<int32_t>(cache_lds / sizeof(float)) : -1;
+    const size_t lds = cache_lds + stash;
     const int block = v.waves_per_block * kWave;
     a.full_rows = a.stride >= v.ne * kWave ? 1 : 0;
     if (lds + v.rec_bytes > 64 * 1024)   // static (records) plus dynamic (cache) LDS above the default limit
