@@ -127,17 +127,22 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
         if (mode == 3) continue;   // windows refilled at the top of the next phase
         const int32_t pl = s_pl, ih = s_ih, a = s_a;
         const int64_t front = s_front;
-        // length of the run: the queue's elements below the other front form a prefix
-        int32_t n = 0;
+        // length of the run: the queue's elements below the other front form a prefix (both queues are in
+        // ascending order). The block narrows [lo, hi] around its end: each round probes the first element
+        // of kMergeThreads equal blocks of the interval, so a run of any length takes a few rounds.
         const int32_t avail = mode == 1 ? V - pl : a - ih;
-        for (int32_t off = 0; off < avail; off += kMergeThreads) {
-            const int32_t q = off + tid;
-            bool ok = false;
-            if (q < avail) ok = mode == 1 ? leaf_val(counts, V, pl + q) <= front : icount[ih + q] < front;
-            const int c = __syncthreads_count(ok);
-            n += c;
-            if (c < kMergeThreads) break;
+        int32_t lo = 0, hi = avail;   // the prefix covers [0, lo) and ends before hi
+        while (lo < hi) {
+            const int32_t step = (hi - lo + kMergeThreads - 1) / kMergeThreads;
+            const int32_t q = lo + tid * step;
+            const bool ok =
+                q < hi && (mode == 1 ? leaf_val(counts, V, pl + q) <= front : icount[ih + q] < front);
+            const int c = __syncthreads_count(ok);   // the probes of blocks 0 .. c-1 lie in the prefix
+            const int32_t nlo = c > 0 ? lo + (c - 1) * step + 1 : lo;
+            hi = min(hi, lo + c * step);
+            lo = nlo;
         }
+        const int32_t n = lo;
         const int32_t m = n / 2;
         if (m == 0) {   // impossible for descending counts (the probe saw a run of kRunMin)
             if (tid == 0) atomicOr(&flags[2], 1);
