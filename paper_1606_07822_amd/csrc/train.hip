@@ -248,15 +248,17 @@ template <int NE, int PG>
 __device__ __forceinline__ void chunk_update(float (&yc)[kChunk][NE], const float (&x)[PG][NE], float (&e)[PG][NE],
                                              int p0, int p1, int nc, int c0, uint64_t code, float alpha,
                                              int lane) {
-    const int bitpos = c0 + (lane >> 4);
-    const float t = (bitpos < 64) ? static_cast<float>((code >> bitpos) & 1ull) : 0.0f;
-    const float one_minus_t = 1.0f - t;
+    // row j's code bit t (lane >> 4 = j; bits past the path only reach rows that are not live), folded
+    // into the gradient g = alpha (1 - t) - alpha sigmoid(z)
+    const uint32_t bits = static_cast<uint32_t>(code >> min(c0, 63));
+    const float a1t = ((bits >> (lane >> 4)) & 1u) ? 0.0f : alpha;
+    const float nalpha = -alpha;
 #pragma unroll
     for (int p = 0; p < PG; ++p) {
         if (p >= p0 && p < p1) {
             const float z = reduce4(dot_partial<NE>(x[p], yc[0]), dot_partial<NE>(x[p], yc[1]),
                                     dot_partial<NE>(x[p], yc[2]), dot_partial<NE>(x[p], yc[3]));
-            const float gr = (one_minus_t - sigmoid_fast(z)) * alpha;
+            const float gr = fmaf(sigmoid_fast(z), nalpha, a1t);
 #pragma unroll
             for (int j = 0; j < kChunk; ++j) {
                 if (j < nc) {
@@ -328,19 +330,18 @@ __device__ __forceinline__ void walk_chunk_buf(const TrainArgs &a, float *val, f
                                                float (&e)[PG][NE], int p0, int p1, int my_pt, int c0, int len,
                                                uint64_t code, float alpha, int lane) {
     load_chunk_buf<NE>(nxt, a, my_pt, c0 + kChunk, len, lane);
+    int node[kChunk];   // read once, used by the LDS fill and the write-back
 #pragma unroll
     for (int j = 0; j < kChunk; ++j) {
-        if (c0 + j < len) {
-            const int n = __builtin_amdgcn_readlane(my_pt, c0 + j);
-            if (n >= a.cache_first)
-                load_row_lds<NE>(cur[j], val + (n - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
-        }
+        node[j] = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
+        if (c0 + j < len && node[j] >= a.cache_first)
+            load_row_lds<NE>(cur[j], val + (node[j] - a.cache_first) * lds_stride<NE>(a.dim), lane, a.dim);
     }
     const int nc = min(kChunk, len - c0);
     chunk_update<NE, PG>(cur, x, e, p0, p1, nc, c0, code, alpha, lane);
 #pragma unroll
     for (int j = 0; j < kChunk; ++j) {
-        const int n = __builtin_amdgcn_readlane(my_pt, min(c0 + j, kWave - 1));
+        const int n = node[j];
         const bool live = j < nc;
         if (live && n >= a.cache_first)
             store_row_lds<NE>(val + (n - a.cache_first) * lds_stride<NE>(a.dim), cur[j], lane, a.dim);
@@ -667,7 +668,7 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
     extern __shared__ float lds[];
     float *val = lds;
     float *orig = lds + a.cache_k * LS;
-    __shared__ int s_centres;
+    __shared__ unsigned s_centres;   // centres of the workgroup since its last write-back, modulo flush_every
     __shared__ int s_lock;
     constexpr bool kRec = rec_slots<NE>();
     __shared__ int4 s_rec[kRec ? WPB : 1][kRec ? kSegLen : 1];   // per wave: its current segment's centre records
@@ -918,10 +919,12 @@ __global__ __launch_bounds__(WPB *kWave) void k_train(TrainArgs a) {
                     n_pairs += P;
                 }
                 if (a.cache_k > 0) {
+                    // the counter wraps at flush_every (ds_inc), so the increment that completes a multiple
+                    // of flush_every centres returns flush_every - 1
                     int go = 0;
                     if (lane == 0) {
-                        const int c = atomicAdd(&s_centres, 1) + 1;
-                        if (c % a.flush_every == 0) go = (atomicCAS(&s_lock, 0, 1) == 0) ? 1 : 0;
+                        const unsigned c = atomicInc(&s_centres, static_cast<unsigned>(a.flush_every - 1));
+                        if (c == static_cast<unsigned>(a.flush_every - 1)) go = (atomicCAS(&s_lock, 0, 1) == 0) ? 1 : 0;
                     }
                     go = __builtin_amdgcn_readfirstlane(go);
                     if (go) {
