@@ -62,6 +62,9 @@ def parse():
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--span-refresh", type=int, default=0,
                     help="words below this index leave the word-row span and are read again after every centre")
+    ap.add_argument("--span-stash", type=int, default=0, choices=(0, 1),
+                    help="1: the re-entering centre row of the word-row span waits in LDS instead of being read "
+                         "again from memory")
     ap.add_argument("--no-loglik", action="store_true", help="leave the held-out log-likelihood out of the step")
     ap.add_argument("--no-probe", action="store_true", help="skip the random-row memory probe")
     ap.add_argument("--sweep-cache", action="store_true",
@@ -156,7 +159,7 @@ def main():
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, arch=w.arch, corpus_tokens=w.n_tokens,
                    seed=synth.SEED_TRAIN, cache_k=args.cache_k, flush_every=args.flush_every,
                    flush_policy=args.flush_policy, write_policy=args.write_policy, workers=args.workers,
-                   cache_mode=args.cache_mode, span_refresh=args.span_refresh)
+                   cache_mode=args.cache_mode, span_refresh=args.span_refresh, span_stash=args.span_stash)
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL, arch=w.arch)
     # held-out tokens as vocabulary indices (input preparation; the vocabulary is the same every step)
     held = torch.from_numpy(voc.id_to_vocab.cpu().numpy()[held_np]).to(dev)
@@ -241,7 +244,8 @@ def main():
     node_gbps = node_bytes / (kernel_ms / 1e3) / 1e9
     res = w2v.last_train_resources()
     cfg_keys = {"cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
-                "write_policy": args.write_policy, "cache_mode": args.cache_mode, "span_refresh": args.span_refresh}
+                "write_policy": args.write_policy, "cache_mode": args.cache_mode, "span_refresh": args.span_refresh,
+                "span_stash": args.span_stash}
     traffic = None
     tfile = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
     if os.path.exists(tfile):
@@ -285,6 +289,7 @@ def main():
                    "window": w.window, "sample": w.sample, "min_count": w.min_count, "epochs_per_step": 1,
                    "cache_k": args.cache_k, "flush_every": args.flush_every, "flush_policy": args.flush_policy,
                    "write_policy": args.write_policy, "cache_mode": args.cache_mode, "span_refresh": args.span_refresh,
+                   "span_stash": args.span_stash,
                    "step": "model reset + vocab + huffman + epoch" +
                    ("" if args.no_loglik else " + held-out loglik")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -168,7 +168,14 @@ typedef struct {
                                 (the most frequent) are written back, if changed, and read again after every
                                 centre while they stay in the span, so that other wavefronts' updates to them
                                 are lost for one centre at most, as without bit 3; 0 = off; >= 0 */
-    int32_t reserved2[2];
+    int32_t span_stash;      /* with write_policy bit 3 in effect: 1 = the row of the word that
+                                becomes the next centre waits in a per-wavefront LDS row while that word is the
+                                centre, and re-enters the span from there instead of from memory (one row read
+                                less per centre when the row fits beside the cache), so other wavefronts'
+                                updates to it during that centre are lost when it is stored again; 0 = off
+                                (the default: with many wavefronts it lowers the held-out log-likelihood and
+                                widens its run-to-run spread); 0 or 1 */
+    int32_t reserved2;
 } w2v_params;
 
 /* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,

@@ -22,7 +22,7 @@ int run_sample_pairs(const int32_t *, int64_t, int32_t, const int64_t *, int64_t
 size_t train_lds_bytes(int32_t cache_k, int32_t dim, bool delta);
 int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int workers, int64_t n_units, int *grid,
                        int *waves,
-                       bool slide = false);
+                       bool slide = false, bool stash = false);
 int64_t train_egrad_floats(int arch, int dim, bool buf, int stride, int window, int waves);
 int train_word_span(int arch, int dim, bool buf, int write_policy, int window);
 int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s,
@@ -155,6 +155,7 @@ int check_params(const w2v_params *p, bool training) {
         if (p->cache_mode != 0 && p->cache_mode != 1) return fail(W2V_E_ARG, "cache_mode must be 0 or 1");
         if (p->hot_k < 0) return fail(W2V_E_ARG, "hot_k must be >= 0");
         if (p->span_refresh < 0) return fail(W2V_E_ARG, "span_refresh must be >= 0");
+        if (p->span_stash != 0 && p->span_stash != 1) return fail(W2V_E_ARG, "span_stash must be 0 or 1");
     }
     return W2V_OK;
 }
@@ -378,6 +379,7 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     a.workers = p->workers;
     a.cache_delta = (p->cache_mode == 1 && p->cache_k > 0) ? 1 : 0;
     a.span_refresh = p->span_refresh;
+    a.span_stash = p->span_stash;
     a.write_policy = kernel_write_policy(p);
     a.stores_only = train_stores_only(a.write_policy, p->cache_k, p->hot_k, m->dim) ? 1 : 0;
     a.flush_scale = p->flush_policy == 1 ? 0.0f : 1.0f;   // 0: set to 1 / workgroups at launch

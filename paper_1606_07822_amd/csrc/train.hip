@@ -1016,8 +1016,9 @@ size_t train_lds_bytes(int32_t cache_k, int32_t dim, bool delta) {
     return (delta ? 1ull : 2ull) * cache_k * v.ls(dim) * sizeof(float) + static_cast<size_t>(v.rec_bytes);
 }
 
-// Dynamic LDS of the word-row span's stash (one row per wavefront) when it fits beside the cache and the
-// centre records; 0 otherwise (the span then reads the re-entering centre word from memory).
+// Dynamic LDS of the word-row span's stash (one row per wavefront) when it is asked for (span_stash) and
+// fits beside the cache and the centre records; 0 otherwise (the span then reads the re-entering centre
+// word from memory).
 size_t span_stash_bytes(const Variant &v, size_t cache_lds, bool slide) {
     if (!slide) return 0;
     const size_t b = static_cast<size_t>(v.waves_per_block) * v.ne * kWave * sizeof(float);
@@ -1025,7 +1026,7 @@ size_t span_stash_bytes(const Variant &v, size_t cache_lds, bool slide) {
 }
 
 int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int workers, int64_t n_units, int *grid,
-                       int *waves, bool slide) {
+                       int *waves, bool slide, bool stash) {
     const Variant v = pick_variant(arch, dim, buf, slide);
     if (workers > 0) {
         *grid = static_cast<int>(ceil_div(workers, v.waves_per_block));
@@ -1033,7 +1034,7 @@ int train_launch_shape(int arch, int dim, int cache_k, bool delta, bool buf, int
         return W2V_OK;
     }
     const size_t cache_lds = (delta ? 1ull : 2ull) * cache_k * v.ls(dim) * sizeof(float);
-    const size_t lds = cache_lds + span_stash_bytes(v, cache_lds, slide);
+    const size_t lds = cache_lds + span_stash_bytes(v, cache_lds, slide && stash);
     int per_cu = 0;
     W2V_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(v.fn),
                                                          v.waves_per_block * kWave, lds));
@@ -1071,7 +1072,7 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
     const bool slide = train_slide(arch, a.dim, a.stores_only != 0, a.write_policy, window);
     const Variant v = pick_variant(arch, a.dim, a.stores_only != 0, slide);
     const size_t cache_lds = (a.cache_delta ? 1ull : 2ull) * a.cache_k * v.ls(a.dim) * sizeof(float);
-    const size_t stash = span_stash_bytes(v, cache_lds, slide);
+    const size_t stash = span_stash_bytes(v, cache_lds, slide && a.span_stash != 0);
     a.stash_off = stash ? static_cast<int32_t>(cache_lds / sizeof(float)) : -1;
     const size_t lds = cache_lds + stash;
     const int block = v.waves_per_block * kWave;
@@ -1081,7 +1082,7 @@ int launch_train_async(TrainArgs a, int arch, int window, hipEvent_t ev0, hipEve
                                     static_cast<int>(lds)));
     int grid = 0, waves = 0;
     if (int rc = train_launch_shape(arch, a.dim, a.cache_k, a.cache_delta != 0, a.stores_only != 0, a.workers,
-                                    a.n_units, &grid, &waves, slide))
+                                    a.n_units, &grid, &waves, slide, a.span_stash != 0))
         return rc;
     a.workers = waves;
     if (train_egrad_floats(arch, a.dim, a.stores_only != 0, a.stride, window, waves) > 0) {

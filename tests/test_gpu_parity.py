@@ -372,6 +372,34 @@ def test_single_worker_word_rows_kept_across_centres(w2v, arch, name, sample, k,
     np.testing.assert_array_equal(g0[untouched], syn0[untouched])
 
 
+# With span_stash the row of the word that becomes the next centre waits in LDS and re-enters the span from
+# there; one wavefront holds the only copy that changes, so it still reproduces the centre-major oracle
+# (repeated words included: the tiny corpus without subsampling repeats words in most spans).
+@pytest.mark.parametrize("arch,name,sample,k,dim", [
+    (0, "tiny_sg_v1k_d50", 0.0, 31, 300), (0, "sg_v30k_d100", 1e-3, 31, 300), (0, "sg_v30k_d100", 1e-3, 0, 200),
+    (1, "tiny_sg_v1k_d50", 0.0, 31, 300), (0, "tiny_sg_v1k_d50", 0.0, 54, 300),
+])
+def test_single_worker_span_stash_matches_oracle(w2v, arch, name, sample, k, dim):
+    log(f"span stash arch={arch} {name} t={sample} k={k} dim={dim}")
+    s = oracle_side(name)
+    voc, tree = gpu_side(w2v, s)
+    tv = s.tv[:3000]
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
+    alpha0 = 0.05 if arch else 0.025
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, dim, window=5, sample=sample, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, cache_k=k, flush_every=10, order=1, arch=arch, alpha0=alpha0)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=sample, corpus_tokens=s.tv.size, cache_k=k, flush_every=10, workers=1,
+                   write_policy=15, arch=arch, alpha0=alpha0, span_stash=1)
+    assert w2v.train_word_span(model, p) == 5
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
 # span_refresh writes the span's frequent words back and reads them again after every centre. One wavefront
 # reads what it wrote, so it still reproduces the centre-major oracle; the result can differ from the run
 # without it in rounding only (slots holding the same word take each other's changes in different orders, and
@@ -464,10 +492,12 @@ def golden(name):
     ("sg_v100k_d200", dict(write_policy=1), 0.9),
     ("sg_v100k_d200", dict(write_policy=7), 0.9),
     ("sg_v100k_d200", dict(write_policy=15), 0.9),
+    ("sg_v100k_d200", dict(write_policy=15, span_stash=1), 0.9),
     ("sg_v100k_d200", dict(cache_mode=1), 0.9),
     ("cbow_v100k_d300", {}, 0.9),
     ("cbow_v100k_d300", dict(write_policy=7), 0.9),
     ("cbow_v100k_d300", dict(write_policy=15), 0.9),
+    ("cbow_v100k_d300", dict(write_policy=15, span_stash=1), 0.9),
 ])
 def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw, min_frac):
     log(f"async LL {name} {kw}")
