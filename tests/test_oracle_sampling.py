@@ -67,6 +67,20 @@ def test_keep_rate_matches_keep_probability():
     assert (np.diff(thr.astype(np.float64)) >= 0).all()   # rarer words are kept more often
 
 
+def test_keep_thresholds_exact_where_the_probability_is_a_dyadic_fraction():
+    """The keep probability min(1, sqrt(q) + q), q = t N / count, in units of 2^-32, at counts where q is
+    a power of two so that sqrt(q) + q is exact: t = 0.25, N = 100 (q = 1/4, 1/16, 1/64, 1, 1/2, 4)."""
+    counts = np.array([100, 400, 1600, 25, 50, 6, 6400], dtype=np.int64)
+    thr = oracle.keep_thresholds(counts, 0.25, 100)
+    assert list(thr) == [3 << 30,                  # 1/2 + 1/4 = 3/4
+                         5 << 28,                  # 1/4 + 1/16 = 5/16
+                         9 << 26,                  # 1/8 + 1/64 = 9/64
+                         1 << 32, 1 << 32,         # q = 1: 2; q = 1/2: 1.207..., kept always
+                         1 << 32,                  # q = 25/6 > 1
+                         (1 << 32) // 16 + (1 << 32) // 256]   # q = 1/256: 1/16 + 1/256
+    assert list(oracle.keep_thresholds(counts, 0.0, 100)) == [1 << 32] * counts.size   # t = 0: keep all
+
+
 def kept_runs(tv, mask, doc_len):
     """Per document, the global raw indices of kept tokens."""
     out = []
