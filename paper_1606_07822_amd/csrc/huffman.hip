@@ -65,9 +65,13 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
             int32_t pl = lb, ih = ib, a = a0;
             int mode = 0;   // 0 done, 1 leaf run, 2 inner run, 3 refill the windows
             int64_t front = 0;
-            // queue values by position / index; callers stay inside the windows (checked below)
-            auto leafv = [&](int32_t q) { return s_leaf[q - lb]; };
-            auto innerv = [&](int32_t q) { return q < a0 ? s_inner[q - ib] : s_new[q - a0]; };
+            // queue values by position / index. The positions a merge uses lie inside the windows (checked
+            // below); the reads are clamped to the windows so that all of a merge's reads can be issued
+            // before any branch on their values (a clamped value is never used).
+            auto leafv = [&](int32_t q) { return s_leaf[min(max(q - lb, 0), kWin - 1)]; };
+            auto innerv = [&](int32_t q) {
+                return q < a0 ? s_inner[min(max(q - ib, 0), kWin - 1)] : s_new[min(q - a0, kWin - 1)];
+            };
             while (a < V - 1) {
                 // this merge reads leaves pl .. pl+2kRunMin-1 and inner nodes ih .. min(ih+2kRunMin, a)-1 at most,
                 // and writes new count a
@@ -80,36 +84,40 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
                     break;
                 }
                 const int32_t nl = V - pl, ni = a - ih;
-                const int64_t FI = ni > 0 ? innerv(ih) : 0;
-                const int64_t FL = nl > 0 ? leafv(pl) : 0;
-                if (ni > 0 && nl >= 2 * kRunMin && leafv(pl + 2 * kRunMin - 1) <= FI) {
+                // both fronts, the elements behind them and the run probes, read together (one LDS round
+                // trip per merge instead of a chain of dependent reads)
+                const int64_t fi = innerv(ih), fl = leafv(pl), i1 = innerv(ih + 1), l1 = leafv(pl + 1);
+                const int64_t probe_l = leafv(pl + 2 * kRunMin - 1), probe_i = innerv(ih + 2 * kRunMin - 1);
+                const int64_t FI = ni > 0 ? fi : 0;
+                const int64_t FL = nl > 0 ? fl : 0;
+                const int64_t I1 = ni > 1 ? i1 : 0;
+                const int64_t L1 = nl > 1 ? l1 : 0;
+                if (ni > 0 && nl >= 2 * kRunMin && probe_l <= FI) {
                     mode = 1;
                     front = FI;
                     break;
                 }
-                if (ni >= 2 * kRunMin && (nl == 0 || innerv(ih + 2 * kRunMin - 1) < FL)) {
+                if (ni >= 2 * kRunMin && (nl == 0 || probe_i < FL)) {
                     mode = 2;
                     front = nl > 0 ? FL : INT64_MAX;
                     break;
                 }
-                // one merge: a leaf wins a tie
-                int64_t sum = 0;
-#pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    const bool use_leaf = pl < V && (ih >= a || leafv(pl) <= innerv(ih));
-                    int32_t child;
-                    if (use_leaf) {
-                        sum += leafv(pl);
-                        child = V - 1 - pl;
-                        ++pl;
-                    } else {
-                        sum += innerv(ih);
-                        child = V + ih;
-                        ++ih;
-                    }
-                    parent[child] = a;
-                    bit[child] = static_cast<uint8_t>(b);
-                }
+                // one merge: a leaf wins a tie; the second pick compares the fronts left by the first
+                const bool leaf0 = nl > 0 && (ni == 0 || FL <= FI);
+                const int32_t nl1 = leaf0 ? nl - 1 : nl, ni1 = leaf0 ? ni : ni - 1;
+                const int64_t fl1 = leaf0 ? L1 : FL, fi1 = leaf0 ? FI : I1;
+                const bool leaf1 = nl1 > 0 && (ni1 == 0 || fl1 <= fi1);
+                const int32_t child0 = leaf0 ? V - 1 - pl : V + ih;
+                if (leaf0) ++pl;
+                else ++ih;
+                const int32_t child1 = leaf1 ? V - 1 - pl : V + ih;
+                if (leaf1) ++pl;
+                else ++ih;
+                const int64_t sum = (leaf0 ? FL : FI) + (leaf1 ? fl1 : fi1);
+                parent[child0] = a;
+                bit[child0] = 0;
+                parent[child1] = a;
+                bit[child1] = 1;
                 icount[a] = sum;
                 s_new[a - a0] = sum;
                 ++a;
