@@ -1,0 +1,63 @@
+"""The whole 1e9-token epoch (V = 1M, d = 300) in the launch configuration that the benchmark times,
+against the sequential oracle's result for the same epoch (Algorithm 1, top-31 cache, u = 10;
+tests/golden/oracle_ll_sg_v1m_d300.json): its counters equal the oracle's, the untrained model's
+held-out log-likelihood equals its closed form, and the trained one is within 1 % of the oracle's and
+keeps most of its gain over the untrained model.
+
+Kept in a file of its own that runs after the other GPU tests: it is the one asynchronous full-size
+run, whose result varies from run to run.
+"""
+import math
+
+import pytest
+
+import oracle
+import synth
+from gpu_common import corpus, ll_gate, log
+from test_gpu_full_size import NAME, golden, gpu_full, oracle_full, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def w2v():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1606_07822_amd as w2v
+    w2v.lib()
+    return w2v
+
+
+def test_full_epoch_in_bench_launch(w2v):
+    """One asynchronous epoch over the whole corpus with the benchmark's settings and launch."""
+    import torch
+    g = golden(f"oracle_sampler_{NAME}.json")
+    w, _, ov, ot = oracle_full()
+    voc, tree = gpu_full(w2v)
+    syn0, syn1 = synth.init_weights(voc.V, w.dim)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    del syn0, syn1
+    held = to_dev(oracle.remap(corpus(NAME, heldout=True), ov.id_to_vocab))
+    pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
+    s0, npairs, nnodes = w2v.hs_loglik(model, held, pe)
+    assert abs(s0 + math.log(2.0) * nnodes) <= 1e-9 * nnodes      # syn1 = 0: every node gives log(1/2)
+    # bench.py's settings: every row stored, word rows kept across centres (write_policy 15)
+    p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
+                   seed=synth.SEED_TRAIN, write_policy=15)
+    assert w2v.train_word_span(model, p) == 5
+    st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
+    grid, waves = w2v.last_train_launch()
+    log(f"  launch {grid} workgroups, {waves} wavefronts, {w2v.last_train_kernel_ms():.0f} ms")
+    assert waves == grid * 12 and grid >= 256
+    assert list(st) == [w.n_tokens, ov.train_words, g["kept"], g["pairs"], g["pair_node_updates"]]
+    s1, np1, _ = w2v.hs_loglik(model, held, pe)
+    assert np1 == npairs
+    syn0_, syn1_ = model.vectors()
+    assert bool(torch.isfinite(syn0_).all()) and bool(torch.isfinite(syn1_).all())
+    log(f"  held-out mean LL {s0 / npairs:.5f} -> {s1 / np1:.5f}")
+    # the quality gate: within 1 % of the sequential oracle's full epoch (Algorithm 1, top-31 cache, u = 10)
+    ref = golden(f"oracle_ll_{NAME}.json")
+    assert (ref["V"], ref["train_words"], ref["heldout_pairs"]) == (ov.V, ov.train_words, npairs)
+    assert abs(ref["init_mean_ll"] - s0 / npairs) <= 1e-9 * abs(s0 / npairs)
+    ll_gate(s1 / np1, ref["mean_ll"], ref["init_mean_ll"])
