@@ -265,14 +265,16 @@ def make_model(syn0_init, syn1_init, vocab: Vocab, tree: Tree, device="cuda", st
 
 # CBOW applies one update per node and centre, so its row stores lose more of
 # the contended upper nodes' changes than skip-gram's; by default those rows
-# take atomic adds there.
+# take atomic adds there -- except with the word-row span (write_policy bit 3),
+# where the stored rows measured both faster and no worse (1e8 tokens, d = 300:
+# 254 instead of 488 ms, held-out CBOW objective -10.066 instead of -10.096).
 HOT_K_CBOW = 1024
 
 
 @dataclass
 class Params:
     """Fields of w2v_params (include/w2v.h). hot_k=None picks 0 for skip-gram
-    and HOT_K_CBOW for CBOW."""
+    and HOT_K_CBOW for CBOW (0 for CBOW with the word-row span, write_policy bit 3)."""
     window: int
     sample: float = 0.0
     alpha0: float = 0.025
@@ -307,7 +309,7 @@ class Params:
     def resolved_hot_k(self) -> int:
         if self.hot_k is not None:
             return self.hot_k
-        return HOT_K_CBOW if self.arch == 1 else 0
+        return HOT_K_CBOW if self.arch == 1 and not (self.write_policy & 8) else 0
 
 
 # ---------------------------------------------------------------- training

@@ -372,6 +372,31 @@ def test_single_worker_word_rows_kept_across_centres(w2v, arch, name, sample, k,
     np.testing.assert_array_equal(g0[untouched], syn0[untouched])
 
 
+# CBOW with the word-row span takes hot_k 0 by default (the store-only walk); with hot rows that take atomic
+# adds it walks the general path, which one worker must match too.
+@pytest.mark.parametrize("name,sample,k,dim", [
+    ("tiny_sg_v1k_d50", 0.0, 31, 300), ("sg_v30k_d100", 1e-3, 31, 300), ("sg_v30k_d100", 1e-3, 0, 256),
+])
+def test_single_worker_cbow_span_with_hot_rows(w2v, name, sample, k, dim):
+    log(f"CBOW span with hot rows {name} t={sample} k={k} dim={dim}")
+    s = oracle_side(name)
+    voc, tree = gpu_side(w2v, s)
+    tv = s.tv[:3000]
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, dim, window=5, sample=sample, train_words=s.voc.train_words,
+                       corpus_tokens=s.tv.size, cache_k=k, flush_every=10, order=1, arch=1, alpha0=0.05)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=sample, corpus_tokens=s.tv.size, cache_k=k, flush_every=10, workers=1,
+                   write_policy=15, arch=1, alpha0=0.05, hot_k=1024)
+    assert w2v.train_word_span(model, p) == 5
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
 # With span_stash the row of the word that becomes the next centre waits in LDS and re-enters the span from
 # there; one wavefront holds the only copy that changes, so it still reproduces the centre-major oracle
 # (repeated words included: the tiny corpus without subsampling repeats words in most spans).
@@ -498,6 +523,7 @@ def golden(name):
     ("cbow_v100k_d300", dict(write_policy=7), 0.9),
     ("cbow_v100k_d300", dict(write_policy=15), 0.9),
     ("cbow_v100k_d300", dict(write_policy=15, span_stash=1), 0.9),
+    ("cbow_v100k_d300", dict(write_policy=15, hot_k=1024), 0.9),
 ])
 def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw, min_frac):
     log(f"async LL {name} {kw}")
