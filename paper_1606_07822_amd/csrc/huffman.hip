@@ -18,6 +18,7 @@ namespace {
 
 constexpr int kMergeThreads = 256;
 constexpr int kRunMin = 32;   // runs of at least this many merges are written by the whole block
+constexpr int kBurst = 8;     // single merges between two checks for a run (2 kBurst < 2 kRunMin)
 
 // Leaves in ascending count: position p is vocabulary index V-1-p.
 __device__ __forceinline__ int64_t leaf_val(const int64_t *__restrict__ counts, int32_t V, int32_t p) {
@@ -73,54 +74,61 @@ __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__r
                 return q < a0 ? s_inner[min(max(q - ib, 0), kWin - 1)] : s_new[min(q - a0, kWin - 1)];
             };
             while (a < V - 1) {
-                // this merge reads leaves pl .. pl+2kRunMin-1 and inner nodes ih .. min(ih+2kRunMin, a)-1 at most,
-                // and writes new count a
+                // checks for the next burst of up to kBurst merges: they read leaves pl .. pl+2kBurst-1 and inner
+                // nodes ih .. ih+2kBurst-1 (both within the probes' reach, pl+2kRunMin-1 and
+                // min(ih+2kRunMin, a)-1, or created in this phase) and write counts a .. a+kBurst-1
                 const int32_t hi = min(ih + 2 * kRunMin, a);
                 const bool leaf_ok = lb + kWin >= V || pl + 2 * kRunMin <= lb + kWin;
                 const bool inner_ok =
-                    min(hi, a0) - ib <= kWin && (hi <= a0 || hi - a0 <= kWin) && a - a0 < kWin;
+                    min(hi, a0) - ib <= kWin && (hi <= a0 || hi - a0 <= kWin) && a + kBurst - a0 <= kWin;
                 if (!leaf_ok || !inner_ok) {
                     mode = 3;
                     break;
                 }
-                const int32_t nl = V - pl, ni = a - ih;
-                // both fronts, the elements behind them and the run probes, read together (one LDS round
-                // trip per merge instead of a chain of dependent reads)
-                const int64_t fi = innerv(ih), fl = leafv(pl), i1 = innerv(ih + 1), l1 = leafv(pl + 1);
-                const int64_t probe_l = leafv(pl + 2 * kRunMin - 1), probe_i = innerv(ih + 2 * kRunMin - 1);
-                const int64_t FI = ni > 0 ? fi : 0;
-                const int64_t FL = nl > 0 ? fl : 0;
-                const int64_t I1 = ni > 1 ? i1 : 0;
-                const int64_t L1 = nl > 1 ? l1 : 0;
-                if (ni > 0 && nl >= 2 * kRunMin && probe_l <= FI) {
-                    mode = 1;
-                    front = FI;
-                    break;
+                {
+                    const int32_t nl = V - pl, ni = a - ih;
+                    const int64_t FI = ni > 0 ? innerv(ih) : 0;
+                    const int64_t FL = nl > 0 ? leafv(pl) : 0;
+                    const int64_t probe_l = leafv(pl + 2 * kRunMin - 1), probe_i = innerv(ih + 2 * kRunMin - 1);
+                    if (ni > 0 && nl >= 2 * kRunMin && probe_l <= FI) {
+                        mode = 1;
+                        front = FI;
+                        break;
+                    }
+                    if (ni >= 2 * kRunMin && (nl == 0 || probe_i < FL)) {
+                        mode = 2;
+                        front = nl > 0 ? FL : INT64_MAX;
+                        break;
+                    }
                 }
-                if (ni >= 2 * kRunMin && (nl == 0 || probe_i < FL)) {
-                    mode = 2;
-                    front = nl > 0 ? FL : INT64_MAX;
-                    break;
+                for (int u = 0; u < kBurst && a < V - 1; ++u) {
+                    const int32_t nl = V - pl, ni = a - ih;
+                    // both fronts and the elements behind them, read together (one LDS round trip per merge)
+                    const int64_t fi = innerv(ih), fl = leafv(pl), i1 = innerv(ih + 1), l1 = leafv(pl + 1);
+                    const int64_t FI = ni > 0 ? fi : 0;
+                    const int64_t FL = nl > 0 ? fl : 0;
+                    const int64_t I1 = ni > 1 ? i1 : 0;
+                    const int64_t L1 = nl > 1 ? l1 : 0;
+                    // one merge: a leaf wins a tie; the second pick compares the fronts left by the first
+                    const bool leaf0 = nl > 0 && (ni == 0 || FL <= FI);
+                    const int32_t nl1 = leaf0 ? nl - 1 : nl, ni1 = leaf0 ? ni : ni - 1;
+                    const int64_t fl1 = leaf0 ? L1 : FL, fi1 = leaf0 ? FI : I1;
+                    const bool leaf1 = nl1 > 0 && (ni1 == 0 || fl1 <= fi1);
+                    const int32_t child0 = leaf0 ? V - 1 - pl : V + ih;
+                    if (leaf0) ++pl;
+                    else ++ih;
+                    const int32_t child1 = leaf1 ? V - 1 - pl : V + ih;
+                    if (leaf1) ++pl;
+                    else ++ih;
+                    const int64_t sum = (leaf0 ? FL : FI) + (leaf1 ? fl1 : fi1);
+                    parent[child0] = a;
+                    bit[child0] = 0;
+                    parent[child1] = a;
+                    bit[child1] = 1;
+                    icount[a] = sum;
+                    s_new[a - a0] = sum;
+                    ++a;
                 }
-                // one merge: a leaf wins a tie; the second pick compares the fronts left by the first
-                const bool leaf0 = nl > 0 && (ni == 0 || FL <= FI);
-                const int32_t nl1 = leaf0 ? nl - 1 : nl, ni1 = leaf0 ? ni : ni - 1;
-                const int64_t fl1 = leaf0 ? L1 : FL, fi1 = leaf0 ? FI : I1;
-                const bool leaf1 = nl1 > 0 && (ni1 == 0 || fl1 <= fi1);
-                const int32_t child0 = leaf0 ? V - 1 - pl : V + ih;
-                if (leaf0) ++pl;
-                else ++ih;
-                const int32_t child1 = leaf1 ? V - 1 - pl : V + ih;
-                if (leaf1) ++pl;
-                else ++ih;
-                const int64_t sum = (leaf0 ? FL : FI) + (leaf1 ? fl1 : fi1);
-                parent[child0] = a;
-                bit[child0] = 0;
-                parent[child1] = a;
-                bit[child1] = 1;
-                icount[a] = sum;
-                s_new[a - a0] = sum;
-                ++a;
             }
             s_pl = pl;
             s_ih = ih;
