@@ -57,7 +57,9 @@ def test_full_epoch_in_bench_launch(w2v):
     assert bool(torch.isfinite(syn0_).all()) and bool(torch.isfinite(syn1_).all())
     log(f"  held-out mean LL {s0 / npairs:.5f} -> {s1 / np1:.5f}")
     # the quality gate: within 1 % of the sequential oracle's full epoch (Algorithm 1, top-31 cache, u = 10)
+    # and at least 0.9 of its gain over the untrained model (48 epochs with these settings kept 0.954 to
+    # 0.977 of it: held-out mean LL -11.888 to -11.876 against the oracle's -11.864)
     ref = golden(f"oracle_ll_{NAME}.json")
     assert (ref["V"], ref["train_words"], ref["heldout_pairs"]) == (ov.V, ov.train_words, npairs)
     assert abs(ref["init_mean_ll"] - s0 / npairs) <= 1e-9 * abs(s0 / npairs)
-    ll_gate(s1 / np1, ref["mean_ll"], ref["init_mean_ll"])
+    ll_gate(s1 / np1, ref["mean_ll"], ref["init_mean_ll"], 0.9)
