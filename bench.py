@@ -298,6 +298,8 @@ def main():
         "train_kernel_words_per_s": words / (kernel_ms / 1e3),
         "stats": dict(zip(w2v.STAT_NAMES, map(int, st))),
         "pair_node_updates_per_s": int(st[4]) / (kernel_ms / 1e3),
+        "kept_centres_per_s": int(st[2]) / (kernel_ms / 1e3),
+        "pairs_per_s": int(st[3]) / (kernel_ms / 1e3),
         "algorithmic_bytes_per_launch": byte_model,
         "byte_model_terms": {"node_rows": node_rows, "pairs": pairs, "path_nodes": path_len, "centres": centres,
                              "span_word_rows": word_rows, "cache_fill_and_writeback_bytes": cache_bytes,
