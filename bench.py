@@ -227,6 +227,31 @@ def main():
     words = int(st[1])
     value = words / (ms_per_step / 1e3)
     kernel_ms = sum(kms_all) / len(kms_all)
+    # the step's stages timed one by one in one more step, after the timed ones (synchronising between them)
+    stage_ms = {}
+
+    def lap(name, t):
+        torch.cuda.synchronize()
+        now = time.perf_counter()
+        stage_ms[name] = (now - t) * 1e3
+        return now
+
+    t = time.perf_counter()
+    model.syn0.copy_(init0)
+    model.syn1.copy_(init1)
+    t = lap("model_reset", t)
+    v = w2v.build_vocab(tok, w.vocab, w.min_count)
+    t = lap("vocab", t)
+    tr = w2v.build_huffman(v.vocab_counts)
+    model.tree = tr
+    model.vocab_counts = v.vocab_counts
+    t = lap("huffman", t)
+    w2v.train_hs_epoch(model, v.tokens, p, workspace=ws)
+    t = lap("epoch", t)
+    if not args.no_loglik:
+        w2v.hs_loglik(model, held, pe)
+        t = lap("heldout_loglik", t)
+    del v, tr
 
     # roofline of the training kernel
     d = w.dim
@@ -298,6 +323,7 @@ def main():
         "train_kernel_words_per_s": words / (kernel_ms / 1e3),
         "stats": dict(zip(w2v.STAT_NAMES, map(int, st))),
         "pair_node_updates_per_s": int(st[4]) / (kernel_ms / 1e3),
+        "stage_ms": stage_ms,
         "kept_centres_per_s": int(st[2]) / (kernel_ms / 1e3),
         "pairs_per_s": int(st[3]) / (kernel_ms / 1e3),
         "algorithmic_bytes_per_launch": byte_model,
