@@ -175,7 +175,9 @@ typedef struct {
                                 updates to it during that centre are lost when it is stored again; 0 = off
                                 (the default: with many wavefronts it lowers the held-out log-likelihood and
                                 widens its run-to-run spread); 0 or 1 */
-    int32_t reserved2;
+    int32_t stash_from;      /* with span_stash 1: only words of vocabulary index >= stash_from (the less
+                                frequent ones, whose rows few other wavefronts update meanwhile) re-enter from
+                                the stash; the more frequent ones are read again from memory; >= 0 */
 } w2v_params;
 
 /* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,

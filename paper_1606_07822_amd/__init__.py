@@ -46,7 +46,7 @@ class CParams(ctypes.Structure):
                 ("corpus_tokens", I64), ("first_raw_index", I64), ("seed", U64), ("cache_k", I32),
                 ("flush_every", I32), ("sync_batch", I32), ("workers", I32), ("write_policy", I32),
                 ("flush_policy", I32), ("hot_k", I32), ("negative", I32), ("cache_mode", I32),
-                ("span_refresh", I32), ("span_stash", I32), ("reserved2", I32)]
+                ("span_refresh", I32), ("span_stash", I32), ("stash_from", I32)]
 
 
 assert ctypes.sizeof(CModel) == 80 and ctypes.sizeof(CParams) == 112
@@ -297,6 +297,7 @@ class Params:
     cache_mode: int = 0
     span_refresh: int = 0
     span_stash: int = 0
+    stash_from: int = 0
     extra: dict = field(default_factory=dict)
 
     def c(self) -> CParams:
@@ -304,7 +305,7 @@ class Params:
                        self.epoch, self.n_epochs, 0, self.corpus_tokens, self.first_raw_index, self.seed,
                        self.cache_k, self.flush_every, self.sync_batch, self.workers, self.write_policy,
                        self.flush_policy, self.resolved_hot_k(), self.negative, self.cache_mode, self.span_refresh,
-                       self.span_stash)
+                       self.span_stash, self.stash_from)
 
     def resolved_hot_k(self) -> int:
         if self.hot_k is not None:

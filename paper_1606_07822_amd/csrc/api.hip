@@ -156,6 +156,7 @@ int check_params(const w2v_params *p, bool training) {
         if (p->hot_k < 0) return fail(W2V_E_ARG, "hot_k must be >= 0");
         if (p->span_refresh < 0) return fail(W2V_E_ARG, "span_refresh must be >= 0");
         if (p->span_stash != 0 && p->span_stash != 1) return fail(W2V_E_ARG, "span_stash must be 0 or 1");
+        if (p->stash_from < 0) return fail(W2V_E_ARG, "stash_from must be >= 0");
     }
     return W2V_OK;
 }
@@ -380,6 +381,7 @@ int w2v_train_hs_epoch(const w2v_model *m, const int32_t *tokens, int64_t n_toke
     a.cache_delta = (p->cache_mode == 1 && p->cache_k > 0) ? 1 : 0;
     a.span_refresh = p->span_refresh;
     a.span_stash = p->span_stash;
+    a.stash_from = p->stash_from;
     a.write_policy = kernel_write_policy(p);
     a.stores_only = train_stores_only(a.write_policy, p->cache_k, p->hot_k, m->dim) ? 1 : 0;
     a.flush_scale = p->flush_policy == 1 ? 0.0f : 1.0f;   // 0: set to 1 / workgroups at launch

@@ -590,8 +590,9 @@ __device__ __forceinline__ void span_apply_same(float (&xw)[PG][NE], const float
 // word v and slot PG-1 the word at position j+1+H (w_edge, -1 past the document's end).
 // stash (LDS, one row per wavefront, or null): slot H's row is the next centre's word, which leaves the span
 // now and comes back as slot H-1 at the next shift; its row is kept in the stash meanwhile (stash_w: the
-// word stashed, -1 for none) and taken from there instead of memory, unless another slot holds the word
-// or a slot leaving at that shift wrote it back.
+// word stashed, -1 for none) and taken from there instead of memory, unless another slot holds the word,
+// a slot leaving at that shift wrote it back, or the word is a frequent one (index below stash_from or
+// span_refresh), whose row other wavefronts are likely to have changed meanwhile.
 template <int NE, int PG>
 __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs &a, int &sid, uint32_t &dirty,
                                            int &pairs, int v, int w_edge, int lane, float *stash, int &stash_w) {
@@ -602,7 +603,7 @@ __device__ __forceinline__ void span_shift(float (&xw)[PG][NE], const TrainArgs 
     if (stash) {
         const int w0 = __builtin_amdgcn_readlane(sid, 0), wh = __builtin_amdgcn_readlane(sid, H);
         back_ok = stash_w >= 0 && stash_w == v && !((dirty & 1u) && w0 == v) && !(((dirty >> H) & 1u) && wh == v) &&
-                  !(v < a.span_refresh);
+                  !(v < a.span_refresh) && v >= a.stash_from;
         if (back_ok) {
 #pragma unroll
             for (int i = 0; i < NE; ++i) back[i] = stash[lane + i * kWave];

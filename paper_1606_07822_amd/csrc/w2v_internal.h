@@ -264,6 +264,7 @@ struct TrainArgs {
     int32_t cache_delta;     // delta-only cache: LDS holds the workgroup's change of each cached row only
     int32_t span_refresh;    // word-row span: words below this index are written back and re-read every centre
     int32_t span_stash;      // word-row span: the re-entering centre row may wait in a per-wave LDS row
+    int32_t stash_from;      // word-row span: the stash takes words of vocabulary index >= stash_from only
     int32_t stash_off;       // word-row span: floats into the dynamic LDS of the per-wave stash row (-1: none)
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, node updates

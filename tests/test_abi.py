@@ -45,6 +45,7 @@ def test_struct_layouts_match_header(w2v):
     assert w2v.CParams.seed.offset == 56 and w2v.CParams.write_policy.offset == 80
     assert w2v.CParams.hot_k.offset == 88 and w2v.CParams.cache_mode.offset == 96
     assert w2v.CParams.span_refresh.offset == 100 and w2v.CParams.span_stash.offset == 104
+    assert w2v.CParams.stash_from.offset == 108
     assert ctypes.sizeof(w2v.CParams) == 112
 
 
@@ -123,6 +124,7 @@ def _params(w2v, **kw):
     ({}, dict(cache_mode=2), "cache_mode"),
     ({}, dict(span_refresh=-1), "span_refresh"),
     ({}, dict(span_stash=2), "span_stash"),
+    ({}, dict(stash_from=-1), "stash_from"),
 ])
 def test_train_argument_errors(w2v, mk, pk, msg):
     L = w2v.lib()

@@ -400,12 +400,13 @@ def test_single_worker_cbow_span_with_hot_rows(w2v, name, sample, k, dim):
 # With span_stash the row of the word that becomes the next centre waits in LDS and re-enters the span from
 # there; one wavefront holds the only copy that changes, so it still reproduces the centre-major oracle
 # (repeated words included: the tiny corpus without subsampling repeats words in most spans).
-@pytest.mark.parametrize("arch,name,sample,k,dim", [
-    (0, "tiny_sg_v1k_d50", 0.0, 31, 300), (0, "sg_v30k_d100", 1e-3, 31, 300), (0, "sg_v30k_d100", 1e-3, 0, 200),
-    (1, "tiny_sg_v1k_d50", 0.0, 31, 300), (0, "tiny_sg_v1k_d50", 0.0, 54, 300),
+@pytest.mark.parametrize("arch,name,sample,k,dim,sfrom", [
+    (0, "tiny_sg_v1k_d50", 0.0, 31, 300, 0), (0, "sg_v30k_d100", 1e-3, 31, 300, 0), (0, "sg_v30k_d100", 1e-3, 0, 200, 0),
+    (1, "tiny_sg_v1k_d50", 0.0, 31, 300, 0), (0, "tiny_sg_v1k_d50", 0.0, 54, 300, 0),
+    (0, "tiny_sg_v1k_d50", 0.0, 31, 300, 40), (0, "sg_v30k_d100", 1e-3, 31, 300, 2000),
 ])
-def test_single_worker_span_stash_matches_oracle(w2v, arch, name, sample, k, dim):
-    log(f"span stash arch={arch} {name} t={sample} k={k} dim={dim}")
+def test_single_worker_span_stash_matches_oracle(w2v, arch, name, sample, k, dim, sfrom):
+    log(f"span stash arch={arch} {name} t={sample} k={k} dim={dim} from={sfrom}")
     s = oracle_side(name)
     voc, tree = gpu_side(w2v, s)
     tv = s.tv[:3000]
@@ -417,7 +418,7 @@ def test_single_worker_span_stash_matches_oracle(w2v, arch, name, sample, k, dim
     ost = oracle.train(a0, a1, s.tree, tv, op)
     model = w2v.make_model(syn0, syn1, voc, tree)
     p = w2v.Params(window=5, sample=sample, corpus_tokens=s.tv.size, cache_k=k, flush_every=10, workers=1,
-                   write_policy=15, arch=arch, alpha0=alpha0, span_stash=1)
+                   write_policy=15, arch=arch, alpha0=alpha0, span_stash=1, stash_from=sfrom)
     assert w2v.train_word_span(model, p) == 5
     st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
     assert list(st) == list(ost)
