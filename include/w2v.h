@@ -172,12 +172,13 @@ typedef struct {
                                 becomes the next centre waits in a per-wavefront LDS row while that word is the
                                 centre, and re-enters the span from there instead of from memory (one row read
                                 less per centre when the row fits beside the cache), so other wavefronts'
-                                updates to it during that centre are lost when it is stored again; 0 = off
-                                (the default: with many wavefronts it lowers the held-out log-likelihood and
-                                widens its run-to-run spread); 0 or 1 */
+                                updates to it during that centre are lost when it is stored again (for the
+                                frequent words, with many wavefronts, this lowers the held-out log-likelihood
+                                and widens its run-to-run spread: see stash_from); 0 = off (the default) or 1 */
     int32_t stash_from;      /* with span_stash 1: only words of vocabulary index >= stash_from (the less
                                 frequent ones, whose rows few other wavefronts update meanwhile) re-enter from
-                                the stash; the more frequent ones are read again from memory; >= 0 */
+                                the stash; the more frequent ones are read again from memory (10000 at V = 1M
+                                keeps the log-likelihood of the run without the stash); >= 0 */
 } w2v_params;
 
 /* stats int64[5]: raw tokens, in-vocabulary tokens, kept centre words, (centre, context) pairs,
