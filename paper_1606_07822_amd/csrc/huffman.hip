@@ -3,10 +3,9 @@
 // Construction rule: leaves in ascending count (vocabulary index V-1 first),
 // inner nodes in creation order; each merge takes the smaller front twice, a
 // leaf winning a count tie; the first child taken gets bit 0; merge a creates
-// inner node a (root = V-2). The merge is a sequential chain except where it
-// runs through many equal-kind merges in a row (the tail of a skewed
-// vocabulary); those runs are written by the whole block, the rest by one lane.
-// Parallel kernels then derive codes, offsets and points.
+// inner node a (root = V-2). The chain of merges is split into generations that
+// are each computed in parallel (below). Parallel kernels then derive codes,
+// offsets and points.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -16,184 +15,149 @@
 namespace w2v {
 namespace {
 
-constexpr int kMergeThreads = 256;
-constexpr int kRunMin = 32;   // runs of at least this many merges are written by the whole block
-constexpr int kBurst = 8;     // single merges between two checks for a run (2 kBurst < 2 kRunMin)
+// Generations. Both queues are in ascending order, and the inner queue is first in,
+// first out. Call the inner nodes that exist when a generation starts (indices
+// ih .. a0-1) old. While an old node is still queued, the inner front is an old node,
+// so every pick is the smaller of the leaf front and an old node: the picks are the
+// stable merge S of the leaf queue with the old nodes (a leaf first on a tie), and
+// merge a0+j takes S[2j] (bit 0) and S[2j+1] (bit 1). S ends with the last old node,
+// after the leaves whose count is at most its count. If S has odd length, its last
+// element (the last old node) opens one more merge whose second pick is the smaller of
+// the leaf front and the first node of this generation (node a0), and the next
+// generation starts. A Zipf vocabulary of 1M words takes 26 generations.
+//
+// One block computes a generation in chunks of kChunk elements of S: it copies the next
+// kChunk leaves and old counts to LDS, and thread j finds how many leaves precede
+// element 2j by a binary search on the merge path (the largest i with A[i-1] <= B[2j-i]
+// and B[2j-i-1] < A[i], A the leaves, B the old nodes), then takes its two picks.
+constexpr int kMergeThreads = 1024;
+constexpr int kChunk = 2 * kMergeThreads;   // elements of S per chunk: one merge per thread
+
+__global__ void k_check_descending(const int64_t *__restrict__ counts, int32_t V, int32_t *__restrict__ flags) {
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i + 1 < V && counts[i] < counts[i + 1]) atomicOr(&flags[2], 1);
+}
 
 // Leaves in ascending count: position p is vocabulary index V-1-p.
 __device__ __forceinline__ int64_t leaf_val(const int64_t *__restrict__ counts, int32_t V, int32_t p) {
     return counts[V - 1 - p];
 }
 
-// Two-queue merge, written in phases. While the next merges alternate between the
-// queues, lane 0 performs them one by one. When the next >= kRunMin merges all take
-// two leaves (every leaf up to the 2m-th is <= the inner front, which those merges
-// leave in place) or all take two inner nodes (every one of the next 2m inner nodes
-// is < the leaf front), the block writes the whole run at once: merge a+i takes
-// elements 2i (bit 0) and 2i+1 (bit 1) of that queue. New inner nodes join the back
-// of their queue and never take part in the run that creates them.
-//
-// Lane 0 reads both queues from LDS: each phase starts with the block copying the next
-// kWin leaves and the next kWin inner counts (those created before the phase) into LDS,
-// and the counts lane 0 creates go to a third LDS window as well as to memory. A phase
-// whose merges would reach past a window ends early and the next one refills them.
-constexpr int kWin = 1024;
-
 __global__ __launch_bounds__(kMergeThreads) void k_huff_merge(const int64_t *__restrict__ counts, int32_t V,
                                                               int32_t *__restrict__ parent, uint8_t *__restrict__ bit,
                                                               int64_t *__restrict__ icount, int32_t *__restrict__ flags) {
-    __shared__ int32_t s_pl, s_ih, s_a, s_mode;
-    __shared__ int64_t s_front;
-    __shared__ int64_t s_leaf[kWin];    // leaf values at queue positions [lb, lb + kWin)
-    __shared__ int64_t s_inner[kWin];   // inner counts [ib, ib + kWin), those below a0
-    __shared__ int64_t s_new[kWin];     // inner counts created in this phase: a0, a0 + 1, ...
+    __shared__ int64_t s_leaf[kChunk];    // A: leaf counts at queue positions pl+i0 ..
+    __shared__ int64_t s_old[kChunk];     // B: old inner counts ih+j0 ..
+    if (flags[2]) return;                 // counts not in descending order: no tree
     const int tid = threadIdx.x;
-    if (tid == 0) {
-        s_pl = 0;
-        s_ih = 0;
-        s_a = 0;
-    }
-    __syncthreads();
-    const int64_t max_phases = 4LL * V + 16;   // every phase merges at least once
-    for (int64_t phase = 0; phase < max_phases; ++phase) {
-        const int32_t lb = s_pl, ib = s_ih, a0 = s_a;
-        for (int i = tid; i < kWin; i += kMergeThreads) {
-            s_leaf[i] = lb + i < V ? leaf_val(counts, V, lb + i) : 0;
-            s_inner[i] = ib + i < a0 ? icount[ib + i] : 0;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            int32_t pl = lb, ih = ib, a = a0;
-            int mode = 0;   // 0 done, 1 leaf run, 2 inner run, 3 refill the windows
-            int64_t front = 0;
-            // queue values by position / index. The positions a merge uses lie inside the windows (checked
-            // below); the reads are clamped to the windows so that all of a merge's reads can be issued
-            // before any branch on their values (a clamped value is never used).
-            auto leafv = [&](int32_t q) { return s_leaf[min(max(q - lb, 0), kWin - 1)]; };
-            auto innerv = [&](int32_t q) {
-                return q < a0 ? s_inner[min(max(q - ib, 0), kWin - 1)] : s_new[min(q - a0, kWin - 1)];
-            };
-            while (a < V - 1) {
-                // checks for the next burst of up to kBurst merges: they read leaves pl .. pl+2kBurst-1 and inner
-                // nodes ih .. ih+2kBurst-1 (both within the probes' reach, pl+2kRunMin-1 and
-                // min(ih+2kRunMin, a)-1, or created in this phase) and write counts a .. a+kBurst-1
-                const int32_t hi = min(ih + 2 * kRunMin, a);
-                const bool leaf_ok = lb + kWin >= V || pl + 2 * kRunMin <= lb + kWin;
-                const bool inner_ok =
-                    min(hi, a0) - ib <= kWin && (hi <= a0 || hi - a0 <= kWin) && a + kBurst - a0 <= kWin;
-                if (!leaf_ok || !inner_ok) {
-                    mode = 3;
-                    break;
-                }
-                {
-                    const int32_t nl = V - pl, ni = a - ih;
-                    const int64_t FI = ni > 0 ? innerv(ih) : 0;
-                    const int64_t FL = nl > 0 ? leafv(pl) : 0;
-                    const int64_t probe_l = leafv(pl + 2 * kRunMin - 1), probe_i = innerv(ih + 2 * kRunMin - 1);
-                    if (ni > 0 && nl >= 2 * kRunMin && probe_l <= FI) {
-                        mode = 1;
-                        front = FI;
-                        break;
-                    }
-                    if (ni >= 2 * kRunMin && (nl == 0 || probe_i < FL)) {
-                        mode = 2;
-                        front = nl > 0 ? FL : INT64_MAX;
-                        break;
-                    }
-                }
-                for (int u = 0; u < kBurst && a < V - 1; ++u) {
-                    const int32_t nl = V - pl, ni = a - ih;
-                    // both fronts and the elements behind them, read together (one LDS round trip per merge)
-                    const int64_t fi = innerv(ih), fl = leafv(pl), i1 = innerv(ih + 1), l1 = leafv(pl + 1);
-                    const int64_t FI = ni > 0 ? fi : 0;
-                    const int64_t FL = nl > 0 ? fl : 0;
-                    const int64_t I1 = ni > 1 ? i1 : 0;
-                    const int64_t L1 = nl > 1 ? l1 : 0;
-                    // one merge: a leaf wins a tie; the second pick compares the fronts left by the first
-                    const bool leaf0 = nl > 0 && (ni == 0 || FL <= FI);
-                    const int32_t nl1 = leaf0 ? nl - 1 : nl, ni1 = leaf0 ? ni : ni - 1;
-                    const int64_t fl1 = leaf0 ? L1 : FL, fi1 = leaf0 ? FI : I1;
-                    const bool leaf1 = nl1 > 0 && (ni1 == 0 || fl1 <= fi1);
-                    const int32_t child0 = leaf0 ? V - 1 - pl : V + ih;
-                    if (leaf0) ++pl;
-                    else ++ih;
-                    const int32_t child1 = leaf1 ? V - 1 - pl : V + ih;
-                    if (leaf1) ++pl;
-                    else ++ih;
-                    const int64_t sum = (leaf0 ? FL : FI) + (leaf1 ? fl1 : fi1);
-                    parent[child0] = a;
-                    bit[child0] = 0;
-                    parent[child1] = a;
-                    bit[child1] = 1;
-                    icount[a] = sum;
-                    s_new[a - a0] = sum;
-                    ++a;
-                }
+    // queue state, the same in every thread: leaf front pl, inner front ih, next merge a
+    int32_t pl = 0, ih = 0, a = 0;
+    // a step is a generation's start or a chunk; each chunk and each first merge performs at least one
+    // merge, so a well-formed input takes at most 2(V-1) steps
+    const int64_t max_steps = 2LL * V + 4;
+    int64_t steps = 0;
+    while (a < V - 1) {
+        const int32_t a0 = a, T = a0 - ih;   // old nodes ih .. a0-1
+        if (++steps > max_steps) break;
+        if (T == 0) {   // no inner node yet (the first merge): two leaves
+            if (tid == 0) {
+                parent[V - 1 - pl] = a;
+                bit[V - 1 - pl] = 0;
+                parent[V - 2 - pl] = a;
+                bit[V - 2 - pl] = 1;
+                icount[a] = leaf_val(counts, V, pl) + leaf_val(counts, V, pl + 1);
             }
-            s_pl = pl;
-            s_ih = ih;
-            s_a = a;
-            s_mode = mode;
-            s_front = front;
+            pl += 2;
+            a += 1;
             __threadfence_block();
+            __syncthreads();
+            continue;
         }
-        __syncthreads();
-        const int mode = s_mode;
-        if (mode == 0) return;
-        if (mode == 3) continue;   // windows refilled at the top of the next phase
-        const int32_t pl = s_pl, ih = s_ih, a = s_a;
-        const int64_t front = s_front;
-        // length of the run: the queue's elements below the other front form a prefix (both queues are in
-        // ascending order). The block narrows [lo, hi] around its end: each round probes the first element
-        // of kMergeThreads equal blocks of the interval, so a run of any length takes a few rounds.
-        const int32_t avail = mode == 1 ? V - pl : a - ih;
-        int32_t lo = 0, hi = avail;   // the prefix covers [0, lo) and ends before hi
-        while (lo < hi) {
-            const int32_t step = (hi - lo + kMergeThreads - 1) / kMergeThreads;
-            const int32_t q = lo + tid * step;
-            const bool ok =
-                q < hi && (mode == 1 ? leaf_val(counts, V, pl + q) <= front : icount[ih + q] < front);
-            const int c = __syncthreads_count(ok);   // the probes of blocks 0 .. c-1 lie in the prefix
-            const int32_t nlo = c > 0 ? lo + (c - 1) * step + 1 : lo;
-            hi = min(hi, lo + c * step);
-            lo = nlo;
-        }
-        const int32_t n = lo;
-        const int32_t m = n / 2;
-        if (m == 0) {   // impossible for descending counts (the probe saw a run of kRunMin)
-            if (tid == 0) atomicOr(&flags[2], 1);
-            return;
-        }
-        for (int32_t i = tid; i < m; i += kMergeThreads) {
-            int32_t c0, c1;
-            int64_t v0, v1;
-            if (mode == 1) {
-                c0 = V - 1 - (pl + 2 * i);
-                c1 = c0 - 1;
-                v0 = leaf_val(counts, V, pl + 2 * i);
-                v1 = leaf_val(counts, V, pl + 2 * i + 1);
-            } else {
-                c0 = V + ih + 2 * i;
-                c1 = c0 + 1;
-                v0 = icount[ih + 2 * i];
-                v1 = icount[ih + 2 * i + 1];
+        const int64_t last = icount[a0 - 1];   // count of the last old node
+        int32_t i0 = 0, j0 = 0;                // leaves and old nodes taken in this generation
+        while (j0 < T) {
+            if (++steps > max_steps) break;
+            const int32_t lw = min(kChunk, V - pl - i0), iw = min(kChunk, T - j0);
+            int32_t nle = 0;   // loaded leaves with count <= last
+#pragma unroll
+            for (int r = 0; r < kChunk / kMergeThreads; ++r) {
+                const int32_t t = tid + r * kMergeThreads;
+                int64_t x = 0;
+                if (t < lw) {
+                    x = leaf_val(counts, V, pl + i0 + t);
+                    s_leaf[t] = x;
+                }
+                if (t < iw) s_old[t] = icount[ih + j0 + t];
+                nle += __syncthreads_count(t < lw && x <= last);
             }
-            parent[c0] = a + i;
-            bit[c0] = 0;
-            parent[c1] = a + i;
-            bit[c1] = 1;
-            icount[a + i] = v0 + v1;
+            // elements of S in this chunk: all kChunk, or up to the last old node when it is loaded (the
+            // leaves at most its count come before it; if every loaded leaf does, S reaches past the chunk)
+            const int32_t out = iw == T - j0 ? min(kChunk, iw + nle) : kChunk;
+            const int32_t M = out >> 1;
+            bool leaf0 = false, leaf1 = false;
+            if (tid < M) {
+                const int32_t k = 2 * tid;
+                int32_t lo = max(0, k - iw), hi = min(k, lw);
+                while (lo < hi) {
+                    const int32_t mid = (lo + hi) >> 1;
+                    if (s_leaf[mid] <= s_old[k - mid - 1]) lo = mid + 1;
+                    else hi = mid;
+                }
+                int32_t i = lo;
+                leaf0 = i < lw && (k - i >= iw || s_leaf[min(i, kChunk - 1)] <= s_old[min(k - i, kChunk - 1)]);
+                const int64_t v0 = leaf0 ? s_leaf[i] : s_old[k - i];
+                const int32_t c0 = leaf0 ? V - 1 - (pl + i0 + i) : V + ih + j0 + (k - i);
+                i += leaf0;
+                leaf1 = i < lw &&
+                        (k + 1 - i >= iw || s_leaf[min(i, kChunk - 1)] <= s_old[min(k + 1 - i, kChunk - 1)]);
+                const int64_t v1 = leaf1 ? s_leaf[i] : s_old[k + 1 - i];
+                const int32_t c1 = leaf1 ? V - 1 - (pl + i0 + i) : V + ih + j0 + (k + 1 - i);
+                parent[c0] = a + tid;
+                bit[c0] = 0;
+                parent[c1] = a + tid;
+                bit[c1] = 1;
+                icount[a + tid] = v0 + v1;
+            }
+            __threadfence_block();
+            const int32_t taken = __syncthreads_count(leaf0) + __syncthreads_count(leaf1);
+            a += M;
+            i0 += taken;
+            j0 += 2 * M - taken;
+            if (out & 1) {
+                __syncthreads();   // node a0's count, written by another thread
+                // S ended on the last old node (ih+j0, count `last`) as the first pick of a merge; the second
+                // is the leaf front or the first node of this generation, a leaf winning a tie. Thread 0
+                // decides, and the barrier's count hands the decision to every thread.
+                const int32_t nl = V - pl - i0;
+                const bool fresh = a > a0;
+                int64_t lf = 0, fn = 0;
+                bool leaf_t0 = false;
+                if (tid == 0) {
+                    lf = nl > 0 ? leaf_val(counts, V, pl + i0) : 0;
+                    fn = fresh ? icount[a0] : 0;
+                    leaf_t0 = nl > 0 && (!fresh || lf <= fn);
+                }
+                const bool take_leaf = __syncthreads_count(leaf_t0) != 0;
+                if (tid == 0) {
+                    parent[V + ih + j0] = a;
+                    bit[V + ih + j0] = 0;
+                    const int32_t c1 = take_leaf ? V - 1 - (pl + i0) : V + a0;
+                    parent[c1] = a;
+                    bit[c1] = 1;
+                    icount[a] = last + (take_leaf ? lf : fn);
+                }
+                j0 += 1;
+                if (take_leaf) ++i0;
+                else ++ih;   // node a0 leaves the queue; the generation ends here (j0 == T)
+                ++a;
+                __threadfence_block();
+                __syncthreads();
+            }
         }
-        __threadfence_block();
-        __syncthreads();
-        if (tid == 0) {
-            if (mode == 1) s_pl = pl + 2 * m;
-            else s_ih = ih + 2 * m;
-            s_a = a + m;
-        }
-        __syncthreads();
+        pl += i0;
+        ih += j0;
     }
-    if (tid == 0) atomicOr(&flags[2], 1);   // phase cap reached: malformed counts
+    if (a < V - 1 && tid == 0) atomicOr(&flags[2], 1);   // step cap reached: malformed counts
 }
 
 // codelen / code per leaf; maxlen and error flag (code longer than 64).
@@ -304,6 +268,8 @@ int run_build_huffman(const int64_t *vocab_counts, int32_t V, uint8_t *codelen, 
     const unsigned gv = static_cast<unsigned>(ceil_div(V, 256));
     k_zero_i32<<<1, 64, 0, s>>>(flags, 4);
     k_fill_parent<<<static_cast<unsigned>(ceil_div(2LL * V, 256)), 256, 0, s>>>(parent, 2 * V);
+    k_check_descending<<<gv, 256, 0, s>>>(vocab_counts, V, flags);
+    W2V_LAUNCH_CHECK("k_check_descending");
     k_huff_merge<<<1, kMergeThreads, 0, s>>>(vocab_counts, V, parent, bit, icount, flags);
     W2V_LAUNCH_CHECK("k_huff_merge");
     k_huff_codes<<<gv, 256, 0, s>>>(parent, bit, V, codelen, code, flags);

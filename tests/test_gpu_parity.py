@@ -127,6 +127,19 @@ def test_huffman_zipf_vocab_bit_exact(w2v, V, s, N):
     check_tree(w2v, counts)
 
 
+def test_huffman_counts_out_of_order_is_an_error(w2v):
+    with pytest.raises(w2v.W2VError) as e:
+        w2v.build_huffman(to_dev(np.array([9, 7, 7, 8, 2], np.int64)))
+    assert e.value.code == w2v.W2V_E_ARG
+
+
+@pytest.mark.parametrize("V,seed", [(2049, 7), (4096 + 3, 8), (20_000, 9)])
+def test_huffman_few_distinct_counts_bit_exact(w2v, V, seed):
+    # long generations of equal counts: merges that span several chunks of the parallel merge
+    rng = np.random.default_rng(seed)
+    check_tree(w2v, np.sort(rng.choice([1, 2, 3, 5, 8, 1000], V))[::-1].astype(np.int64))
+
+
 def test_huffman_too_deep_is_an_error(w2v):
     fib = [1, 1]
     while len(fib) < 70:
