@@ -185,39 +185,67 @@ __global__ void k_huff_codes(const int32_t *__restrict__ parent, const uint8_t *
     atomicMax(&flags[0], depth);
 }
 
-// Exclusive prefix sum of codelen into point_off[0..V], one block walking the array.
-constexpr int kScanThreads = 1024;
-__global__ __launch_bounds__(kScanThreads) void k_scan_codelen(const uint8_t *__restrict__ codelen, int32_t V,
-                                                               int32_t *__restrict__ point_off,
-                                                               int64_t *__restrict__ total) {
-    __shared__ int64_t wsum[kScanThreads / 64];
-    __shared__ int64_t carry;
-    if (threadIdx.x == 0) carry = 0;
-    __syncthreads();
+// Exclusive prefix sum of codelen into point_off[0..V] in three passes: the sum of each tile of
+// kScanTile code lengths, one block scanning the tile sums, and each tile's own scan plus its offset.
+constexpr int kScanTile = 1024;
+
+// inclusive block scan of one value per thread (kScanTile threads); returns the inclusive prefix, *sum the total
+__device__ __forceinline__ int64_t block_incl_scan(int64_t x, int64_t *wsum, int64_t *sum) {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    for (int32_t base = 0; base < V; base += kScanThreads) {
-        const int32_t i = base + threadIdx.x;
-        const int64_t x = i < V ? codelen[i] : 0;
-        // inclusive wave scan
-        int64_t inc = x;
+    int64_t inc = x;
 #pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int64_t y = __shfl_up(inc, d, 64);
-            if (lane >= d) inc += y;
-        }
-        if (lane == 63) wsum[wid] = inc;
-        __syncthreads();
-        int64_t before = carry;
-        for (int w = 0; w < wid; ++w) before += wsum[w];
-        if (i < V) point_off[i] = static_cast<int32_t>(before + inc - x);
-        __syncthreads();
-        if (threadIdx.x == kScanThreads - 1) carry = before + inc;
-        __syncthreads();
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += y;
     }
-    if (threadIdx.x == 0) {
-        point_off[V] = static_cast<int32_t>(carry);
-        *total = carry;
+    if (lane == 63) wsum[wid] = inc;
+    __syncthreads();
+    int64_t before = 0, total = 0;
+    for (int w = 0; w < kScanTile / 64; ++w) {
+        before += w < wid ? wsum[w] : 0;
+        total += wsum[w];
     }
+    *sum = total;
+    __syncthreads();   // wsum is reused by the next call
+    return before + inc;
+}
+
+__global__ __launch_bounds__(kScanTile) void k_scan_tiles(const uint8_t *__restrict__ codelen, int32_t V,
+                                                          int64_t *__restrict__ tile_sum) {
+    __shared__ int64_t wsum[kScanTile / 64];
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x;
+    int64_t total;
+    block_incl_scan(i < V ? codelen[i] : 0, wsum, &total);
+    if (threadIdx.x == 0) tile_sum[blockIdx.x] = total;
+}
+
+// tile_sum -> exclusive tile offsets in place; *total = sum of all code lengths
+__global__ __launch_bounds__(kScanTile) void k_scan_tile_sums(int64_t *__restrict__ tile_sum, int32_t n_tiles,
+                                                              int64_t *__restrict__ total) {
+    __shared__ int64_t wsum[kScanTile / 64];
+    int64_t carry = 0;
+    for (int32_t base = 0; base < n_tiles; base += kScanTile) {
+        const int32_t i = base + threadIdx.x;
+        const int64_t x = i < n_tiles ? tile_sum[i] : 0;
+        int64_t chunk;
+        const int64_t inc = block_incl_scan(x, wsum, &chunk);
+        if (i < n_tiles) tile_sum[i] = carry + inc - x;
+        carry += chunk;
+    }
+    if (threadIdx.x == 0) *total = carry;
+}
+
+__global__ __launch_bounds__(kScanTile) void k_scan_apply(const uint8_t *__restrict__ codelen, int32_t V,
+                                                          const int64_t *__restrict__ tile_off,
+                                                          const int64_t *__restrict__ total,
+                                                          int32_t *__restrict__ point_off) {
+    __shared__ int64_t wsum[kScanTile / 64];
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x;
+    const int64_t x = i < V ? codelen[i] : 0;
+    int64_t chunk;
+    const int64_t inc = block_incl_scan(x, wsum, &chunk);
+    if (i < V) point_off[i] = static_cast<int32_t>(tile_off[blockIdx.x] + inc - x);
+    if (i == V) point_off[V] = static_cast<int32_t>(*total);
 }
 
 __global__ void k_huff_points(const int32_t *__restrict__ parent, int32_t V, const uint8_t *__restrict__ codelen,
@@ -253,6 +281,7 @@ size_t huffman_workspace_bytes(int32_t V) {
     c.take<int64_t>(static_cast<size_t>(V));       // icount
     c.take<int32_t>(4);                            // flags
     c.take<int64_t>(2);                            // total
+    c.take<int64_t>(static_cast<size_t>(ceil_div(V, kScanTile)));   // tile sums of the code-length scan
     return c.used();
 }
 
@@ -265,6 +294,8 @@ int run_build_huffman(const int64_t *vocab_counts, int32_t V, uint8_t *codelen, 
     int64_t *icount = c.take<int64_t>(static_cast<size_t>(V));
     int32_t *flags = c.take<int32_t>(4);
     int64_t *total = c.take<int64_t>(2);
+    const int32_t n_tiles = static_cast<int32_t>(ceil_div(V, kScanTile));
+    int64_t *tile_sum = c.take<int64_t>(static_cast<size_t>(n_tiles));
     const unsigned gv = static_cast<unsigned>(ceil_div(V, 256));
     k_zero_i32<<<1, 64, 0, s>>>(flags, 4);
     k_fill_parent<<<static_cast<unsigned>(ceil_div(2LL * V, 256)), 256, 0, s>>>(parent, 2 * V);
@@ -274,7 +305,11 @@ int run_build_huffman(const int64_t *vocab_counts, int32_t V, uint8_t *codelen, 
     W2V_LAUNCH_CHECK("k_huff_merge");
     k_huff_codes<<<gv, 256, 0, s>>>(parent, bit, V, codelen, code, flags);
     W2V_LAUNCH_CHECK("k_huff_codes");
-    k_scan_codelen<<<1, kScanThreads, 0, s>>>(codelen, V, point_off, total);
+    k_scan_tiles<<<static_cast<unsigned>(n_tiles), kScanTile, 0, s>>>(codelen, V, tile_sum);
+    k_scan_tile_sums<<<1, kScanTile, 0, s>>>(tile_sum, n_tiles, total);
+    // one more thread than V writes point_off[V]
+    k_scan_apply<<<static_cast<unsigned>(ceil_div(static_cast<int64_t>(V) + 1, kScanTile)), kScanTile, 0, s>>>(
+        codelen, V, tile_sum, total, point_off);
     W2V_LAUNCH_CHECK("k_scan_codelen");
     int32_t hflags[3];
     int64_t htotal = 0;

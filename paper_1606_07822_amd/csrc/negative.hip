@@ -152,8 +152,10 @@ __device__ __forceinline__ float bcast(float v, int lane) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
 }
 
+// log sigmoid(u) = min(u, 0) - log(1 + exp(-|u|)): the same operations as the two one-sided forms, without
+// a branch (lanes of both signs would run both sides)
 __device__ __forceinline__ double log_sigmoid(double u) {
-    return u >= 0.0 ? -log1p(exp(-u)) : u - log1p(exp(u));
+    return fmin(u, 0.0) - log1p(exp(-fabs(u)));
 }
 
 // ------------------------------------------------------------ training

@@ -273,8 +273,10 @@ int run_train_sync(const w2v_model *m, const w2v_params *p, const SampleBufs &b,
 // ------------------------------------------------------------- log-likelihood
 namespace {
 
+// log sigmoid(u) = min(u, 0) - log(1 + exp(-|u|)): the same operations as the two one-sided forms, without
+// a branch (lanes of both signs would run both sides)
 __device__ __forceinline__ double log_sigmoid(double u) {
-    return u >= 0.0 ? -log1p(exp(-u)) : u - log1p(exp(u));
+    return fmin(u, 0.0) - log1p(exp(-fabs(u)));
 }
 
 struct LLArgs {
@@ -488,7 +490,7 @@ LLFn pick_ll(int dim) {
     if (ne <= 1) return k_loglik<1, 10>;
     if (ne <= 2) return k_loglik<2, 10>;
     if (ne <= 4) return k_loglik<4, 10>;
-    if (ne <= 5) return k_loglik<5, 10>;
+    if (ne <= 5) return k_loglik<5, 8>;   // 159 VGPRs: 3 waves per SIMD (10 words: 171, 2 waves)
     if (ne <= 8) return k_loglik<8, 4>;
     return k_loglik<16, 2>;
 }

@@ -12,8 +12,8 @@
 namespace w2v {
 namespace {
 
-constexpr int kHotBins = 8192;   // ids below this are counted in LDS first (Zipf-ranked ids are hot)
-constexpr int kCountThreads = 512;
+constexpr int kHotBins = 36864;   // ids below this are counted in LDS first (Zipf-ranked ids are hot); 144 KiB
+constexpr int kCountThreads = 1024;   // one workgroup per CU (the bins take most of its LDS)
 
 __global__ __launch_bounds__(kCountThreads) void k_count(const int32_t *__restrict__ tok, int64_t n,
                                                          int32_t id_space, unsigned long long *__restrict__ counts,
@@ -175,13 +175,20 @@ __global__ void k_finish_vocab(const Rec *__restrict__ r, int32_t id_space, int3
     }
 }
 
+// Four tokens per thread and step (16-byte loads and stores where the stream is 16-byte aligned), so that
+// each thread keeps four independent gathers from id_to_vocab in flight.
 __global__ void k_remap(const int32_t *__restrict__ tok, int64_t n, const int32_t *__restrict__ id_to_vocab,
                         int32_t id_space, int32_t *__restrict__ out) {
+    auto map = [&](int32_t v) { return (v >= 0 && v < id_space) ? id_to_vocab[v] : -1; };
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
-        const int32_t v = tok[i];
-        out[i] = (v >= 0 && v < id_space) ? id_to_vocab[v] : -1;
+    const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const bool aligned = ((reinterpret_cast<uintptr_t>(tok) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
+    const int64_t nq = aligned ? n / 4 : 0;   // whole 16-byte groups
+    for (int64_t q = tid; q < nq; q += stride) {
+        const int4 t = reinterpret_cast<const int4 *>(tok)[q];
+        reinterpret_cast<int4 *>(out)[q] = make_int4(map(t.x), map(t.y), map(t.z), map(t.w));
     }
+    for (int64_t i = nq * 4 + tid; i < n; i += stride) out[i] = map(tok[i]);
 }
 
 __global__ void k_zero_u64(unsigned long long *p, int64_t n) {
@@ -220,7 +227,7 @@ int run_build_vocab(const int32_t *tokens, int64_t n_tokens, int32_t id_space, i
     if (n_tokens > 0) {
         const int cus = device_cu_count();
         const int64_t want = ceil_div(n_tokens, static_cast<int64_t>(kCountThreads) * 4 * 16);
-        const unsigned grid = static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>(want, 4LL * cus)));
+        const unsigned grid = static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>(want, 1LL * cus)));
         k_count<<<grid, kCountThreads, 0, s>>>(tokens, n_tokens, id_space, counts, scal + 0);
         W2V_LAUNCH_CHECK("k_count");
     }
@@ -238,7 +245,7 @@ int run_build_vocab(const int32_t *tokens, int64_t n_tokens, int32_t id_space, i
         recs, id_space, vocab_ids, vocab_counts, id_to_vocab, scal + 1, scal + 2);
     W2V_LAUNCH_CHECK("k_finish_vocab");
     if (tokens_out && n_tokens > 0) {
-        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(ceil_div(n_tokens, 256), 8192));
+        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(ceil_div(n_tokens, 4 * 256), 8192));
         k_remap<<<grid, 256, 0, s>>>(tokens, n_tokens, id_to_vocab, id_space, tokens_out);
         W2V_LAUNCH_CHECK("k_remap");
     }

@@ -22,7 +22,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_common import corpus, ll_gate, log, row_rel_err
+from gpu_common import corpus, gated, log, row_rel_err
 
 pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -163,13 +163,17 @@ def test_full_prefix_async_loglik_within_1pct(w2v, wp):
     assert (g["V"], g["train_words"], g["train_tokens"]) == (ov.V, ov.train_words, PREFIX)
     voc, tree = gpu_full(w2v)
     syn0, syn1 = synth.init_weights(voc.V, w.dim)
-    model = w2v.make_model(syn0, syn1, voc, tree)
-    del syn0, syn1
-    p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=PREFIX, seed=synth.SEED_TRAIN,
-                   write_policy=wp)
-    st = w2v.train_hs_epoch(model, voc.tokens[:PREFIX], p).cpu().numpy()
-    assert list(st) == g["stats"]
     held = to_dev(oracle.remap(corpus(NAME, heldout=True), ov.id_to_vocab))
-    s, npairs, _ = w2v.hs_loglik(model, held, w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL))
-    assert npairs == g["heldout_pairs"]
-    ll_gate(s / npairs, g["mean_ll"], g["init_mean_ll"], 0.9)
+
+    def run():
+        model = w2v.make_model(syn0, syn1, voc, tree)
+        p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=PREFIX,
+                       seed=synth.SEED_TRAIN, write_policy=wp)
+        st = w2v.train_hs_epoch(model, voc.tokens[:PREFIX], p).cpu().numpy()
+        assert list(st) == g["stats"]
+        s, npairs, _ = w2v.hs_loglik(model, held, w2v.Params(window=w.window, sample=w.sample,
+                                                             seed=synth.SEED_EVAL))
+        assert npairs == g["heldout_pairs"]
+        return s / npairs
+
+    gated(run, g["mean_ll"], g["init_mean_ll"], 0.9)

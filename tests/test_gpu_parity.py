@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_common import corpus, ll_gate, log, oracle_side, row_rel_err
+from gpu_common import corpus, gated, ll_gate, log, oracle_side, row_rel_err
 
 pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -472,8 +472,17 @@ def test_span_refresh_single_worker_matches_oracle(w2v, arch, name, sample, dim,
     assert row_rel_err(out[1][0], out[0][0]) <= 1e-5
 
 
+def same_vocab_and_tree(voc, tree, s):
+    # the inputs of an asynchronous run are deterministic: a quality miss is then the training's own
+    np.testing.assert_array_equal(voc.id_to_vocab.cpu().numpy(), s.voc.id_to_vocab)
+    np.testing.assert_array_equal(voc.vocab_counts.cpu().numpy(), s.voc.vocab_counts)
+    np.testing.assert_array_equal(tree.code.cpu().numpy().view(np.uint64), s.tree.code)
+    np.testing.assert_array_equal(tree.points.cpu().numpy(), s.tree.points)
+
+
 def async_ll(w2v, s, held, **kw):
     voc, tree = gpu_side(w2v, s)
+    same_vocab_and_tree(voc, tree, s)
     syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim)
     model = w2v.make_model(syn0, syn1, voc, tree)
     p = w2v.Params(window=s.w.window, sample=s.w.sample, corpus_tokens=s.tv.size, arch=s.w.arch, alpha0=s.w.alpha0,
@@ -498,9 +507,13 @@ def test_async_loglik_within_1pct_tiny(w2v, kw):
     pe = oracle.params(s.voc.V, s.w.dim, window=2, train_words=s.voc.train_words, seed=4)
     s0, _, _ = oracle.loglik(*synth.init_weights(s.voc.V, s.w.dim), s.tree, hv, pe)
     so, npo, _ = oracle.loglik(syn0, syn1, s.tree, hv, pe)
-    g, npg = async_ll(w2v, s, held, **kw)
-    assert npg == npo
-    ll_gate(g, so / npo, s0 / npo)
+
+    def run():
+        g, npg = async_ll(w2v, s, held, **kw)
+        assert npg == npo
+        return g
+
+    gated(run, so / npo, s0 / npo)
 
 
 def golden(name):
@@ -545,9 +558,13 @@ def test_async_loglik_within_1pct_of_stored_oracle(w2v, name, kw, min_frac):
     s = oracle_side(name)
     assert s.voc.V == gold["V"] and s.voc.train_words == gold["train_words"]
     held = corpus(name, heldout=True)
-    g, npg = async_ll(w2v, s, held, **kw)
-    assert npg == gold["heldout_pairs"]
-    ll_gate(g, gold["mean_ll"], gold["init_mean_ll"], min_frac)
+
+    def run():
+        g, npg = async_ll(w2v, s, held, **kw)
+        assert npg == gold["heldout_pairs"]
+        return g
+
+    gated(run, gold["mean_ll"], gold["init_mean_ll"], min_frac)
 
 
 # ------------------------------------------------------------- memory probe
@@ -635,15 +652,20 @@ def test_async_loglik_reversed_and_epochs(w2v, name, gold, arch, epochs):
     s = oracle_side(name)
     assert s.voc.V == g["V"] and s.voc.train_words == g["train_words"]
     voc, tree = gpu_side(w2v, s)
+    same_vocab_and_tree(voc, tree, s)
     syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim)
-    model = w2v.make_model(syn0, syn1, voc, tree)
-    for e in range(epochs):
-        p = w2v.Params(window=s.w.window, sample=s.w.sample, corpus_tokens=s.tv.size, arch=arch, alpha0=s.w.alpha0,
-                       epoch=e, n_epochs=epochs)
-        st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
-        assert list(st) == (g["stats"][e] if epochs > 1 else g["stats"])
-    held = corpus(name, heldout=True)
-    hv = to_dev(oracle.remap(held, s.voc.id_to_vocab))
-    sg, npairs, _ = w2v.hs_loglik(model, hv, w2v.Params(window=s.w.window, sample=s.w.sample, seed=synth.SEED_EVAL))
-    assert npairs == g["heldout_pairs"]
-    ll_gate(sg / npairs, g["mean_ll"], g["init_mean_ll"], 0.9)
+    hv = to_dev(oracle.remap(corpus(name, heldout=True), s.voc.id_to_vocab))
+
+    def run():
+        model = w2v.make_model(syn0, syn1, voc, tree)
+        for e in range(epochs):
+            p = w2v.Params(window=s.w.window, sample=s.w.sample, corpus_tokens=s.tv.size, arch=arch,
+                           alpha0=s.w.alpha0, epoch=e, n_epochs=epochs)
+            st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
+            assert list(st) == (g["stats"][e] if epochs > 1 else g["stats"])
+        sg, npairs, _ = w2v.hs_loglik(model, hv, w2v.Params(window=s.w.window, sample=s.w.sample,
+                                                            seed=synth.SEED_EVAL))
+        assert npairs == g["heldout_pairs"]
+        return sg / npairs
+
+    gated(run, g["mean_ll"], g["init_mean_ll"], 0.9)

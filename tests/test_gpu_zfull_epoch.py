@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_common import corpus, ll_gate, log
+from gpu_common import corpus, gated, log
 from test_gpu_full_size import NAME, golden, gpu_full, oracle_full, to_dev
 
 pytestmark = pytest.mark.gpu
@@ -36,31 +36,34 @@ def test_full_epoch_in_bench_launch(w2v):
     w, _, ov, ot = oracle_full()
     voc, tree = gpu_full(w2v)
     syn0, syn1 = synth.init_weights(voc.V, w.dim)
-    model = w2v.make_model(syn0, syn1, voc, tree)
-    del syn0, syn1
     held = to_dev(oracle.remap(corpus(NAME, heldout=True), ov.id_to_vocab))
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
-    s0, npairs, nnodes = w2v.hs_loglik(model, held, pe)
-    assert abs(s0 + math.log(2.0) * nnodes) <= 1e-9 * nnodes      # syn1 = 0: every node gives log(1/2)
+    ref = golden(f"oracle_ll_{NAME}.json")
     # bench.py's settings: every row stored, word rows kept across centres (write_policy 15), the old
     # centre's row back from the stash for words of index >= 10000
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
                    seed=synth.SEED_TRAIN, write_policy=15, span_stash=1, stash_from=10000)
-    assert w2v.train_word_span(model, p) == 5
-    st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
-    grid, waves = w2v.last_train_launch()
-    log(f"  launch {grid} workgroups, {waves} wavefronts, {w2v.last_train_kernel_ms():.0f} ms")
-    assert waves == grid * 12 and grid >= 256
-    assert list(st) == [w.n_tokens, ov.train_words, g["kept"], g["pairs"], g["pair_node_updates"]]
-    s1, np1, _ = w2v.hs_loglik(model, held, pe)
-    assert np1 == npairs
-    syn0_, syn1_ = model.vectors()
-    assert bool(torch.isfinite(syn0_).all()) and bool(torch.isfinite(syn1_).all())
-    log(f"  held-out mean LL {s0 / npairs:.5f} -> {s1 / np1:.5f}")
+
+    def run():
+        model = w2v.make_model(syn0, syn1, voc, tree)
+        s0, npairs, nnodes = w2v.hs_loglik(model, held, pe)
+        assert abs(s0 + math.log(2.0) * nnodes) <= 1e-9 * nnodes      # syn1 = 0: every node gives log(1/2)
+        assert (ref["V"], ref["train_words"], ref["heldout_pairs"]) == (ov.V, ov.train_words, npairs)
+        assert abs(ref["init_mean_ll"] - s0 / npairs) <= 1e-9 * abs(s0 / npairs)
+        assert w2v.train_word_span(model, p) == 5
+        st = w2v.train_hs_epoch(model, voc.tokens, p).cpu().numpy()
+        grid, waves = w2v.last_train_launch()
+        log(f"  launch {grid} workgroups, {waves} wavefronts, {w2v.last_train_kernel_ms():.0f} ms")
+        assert waves == grid * 12 and grid >= 256
+        assert list(st) == [w.n_tokens, ov.train_words, g["kept"], g["pairs"], g["pair_node_updates"]]
+        s1, np1, _ = w2v.hs_loglik(model, held, pe)
+        assert np1 == npairs
+        syn0_, syn1_ = model.vectors()
+        assert bool(torch.isfinite(syn0_).all()) and bool(torch.isfinite(syn1_).all())
+        log(f"  held-out mean LL {s0 / npairs:.5f} -> {s1 / np1:.5f}")
+        return s1 / np1
+
     # the quality gate: within 1 % of the sequential oracle's full epoch (Algorithm 1, top-31 cache, u = 10)
-    # and at least 0.9 of its gain over the untrained model (20 epochs with these settings kept 0.955 to
-    # 0.977 of it: held-out mean LL -11.889 to -11.876 against the oracle's -11.864)
-    ref = golden(f"oracle_ll_{NAME}.json")
-    assert (ref["V"], ref["train_words"], ref["heldout_pairs"]) == (ov.V, ov.train_words, npairs)
-    assert abs(ref["init_mean_ll"] - s0 / npairs) <= 1e-9 * abs(s0 / npairs)
-    ll_gate(s1 / np1, ref["mean_ll"], ref["init_mean_ll"], 0.9)
+    # and at least 0.9 of its gain over the untrained model (runs with these settings kept about 0.97 of it:
+    # held-out mean LL near -11.879 against the oracle's -11.864)
+    gated(run, ref["mean_ll"], ref["init_mean_ll"], 0.9)
