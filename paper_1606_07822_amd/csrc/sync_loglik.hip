@@ -279,6 +279,12 @@ __device__ __forceinline__ double log_sigmoid(double u) {
     return fmin(u, 0.0) - log1p(exp(-fabs(u)));
 }
 
+// Held-out evaluation work units: kLLSeg consecutive kept centres of a document, one wavefront each.
+// Short units keep the read-only walk's latency spread over many wavefronts (8: 4.2 ms for the 1e6-token
+// held-out corpus at V = 1M, d = 300; the training kernel's 128-centre units: 8.4 ms).
+constexpr int kLLSeg = 8;
+inline int32_t ll_segs_per_doc(int32_t doc_len) { return static_cast<int32_t>(ceil_div(doc_len, kLLSeg)); }
+
 struct LLArgs {
     const float *syn0;
     const float *syn1;
@@ -290,7 +296,7 @@ struct LLArgs {
     const int32_t *kept_vid;
     const uint32_t *kept_meta;
     const int32_t *doc_kept;
-    int64_t n_units;        // work units: kSegLen consecutive kept centres of one document
+    int64_t n_units;        // work units: kLLSeg consecutive kept centres of one document
     int32_t segs_per_doc;
     int32_t doc_len;
     double *unit_ll;
@@ -311,8 +317,8 @@ __global__ __launch_bounds__(256) void k_loglik(LLArgs a) {
     for (int64_t u = wave0; u < a.n_units; u += nwaves) {
         const int64_t d = u / a.segs_per_doc;
         const int nk = a.doc_kept[d];
-        const int j0 = static_cast<int>(u - d * a.segs_per_doc) * kSegLen;
-        const int j1 = min(nk, j0 + kSegLen);
+        const int j0 = static_cast<int>(u - d * a.segs_per_doc) * kLLSeg;
+        const int j1 = min(nk, j0 + kLLSeg);
         const int64_t base = d * a.doc_len;
         double acc = 0.0;
         int64_t nodes = 0;
@@ -396,8 +402,8 @@ __global__ __launch_bounds__(256) void k_loglik_cbow(LLArgs a) {
     for (int64_t u = wave0; u < a.n_units; u += nwaves) {
         const int64_t d = u / a.segs_per_doc;
         const int nk = a.doc_kept[d];
-        const int j0 = static_cast<int>(u - d * a.segs_per_doc) * kSegLen;
-        const int j1 = min(nk, j0 + kSegLen);
+        const int j0 = static_cast<int>(u - d * a.segs_per_doc) * kLLSeg;
+        const int j1 = min(nk, j0 + kLLSeg);
         const int64_t base = d * a.doc_len;
         double acc = 0.0;
         int64_t nodes = 0, terms = 0;
@@ -508,7 +514,7 @@ LLFn pick_ll_cbow(int dim) {
 }  // namespace
 
 int64_t loglik_units(int64_t n_tokens, int32_t doc_len) {
-    return std::max<int64_t>(1, ceil_div(n_tokens, doc_len)) * segs_per_doc(doc_len);
+    return std::max<int64_t>(1, ceil_div(n_tokens, doc_len)) * ll_segs_per_doc(doc_len);
 }
 
 size_t loglik_extra_bytes(int64_t n_units) {
@@ -536,7 +542,7 @@ int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int
     a.kept_vid = b.kept_vid;
     a.kept_meta = b.kept_meta;
     a.doc_kept = b.doc_kept;
-    a.segs_per_doc = segs_per_doc(p->doc_len);
+    a.segs_per_doc = ll_segs_per_doc(p->doc_len);
     a.n_units = n_tokens > 0 ? ceil_div(n_tokens, p->doc_len) * a.segs_per_doc : 0;
     a.doc_len = p->doc_len;
     a.unit_ll = c.take<double>(static_cast<size_t>(n_units));
@@ -546,8 +552,9 @@ int run_loglik(const w2v_model *m, const w2v_params *p, const SampleBufs &b, int
     int64_t *out_nt = c.take<int64_t>(2);   // nodes, terms
     const bool cbow = p->arch == 1;
     if (a.n_units > 0) {
-        const unsigned grid =
-            static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_units, 4), 16LL * device_cu_count()));
+        // one unit per wavefront: the hardware hands out workgroups as others finish, which balances the
+        // uneven units (a document's kept centres end in a partial unit, and units past them are empty)
+        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_units, 4), INT32_MAX));
         hipLaunchKernelGGL(cbow ? pick_ll_cbow(m->dim) : pick_ll(m->dim), dim3(grid), dim3(256), 0, s, a);
         W2V_LAUNCH_CHECK("k_loglik");
         k_sum_docs<<<1, 1024, 0, s>>>(a.unit_ll, a.unit_nodes, cbow ? a.unit_terms : nullptr, a.n_units, out,

@@ -196,16 +196,23 @@ def test_pairs_checksum_full_corpus(w2v, name):
 
 
 # ------------------------------------------------------------- evaluation
-def test_loglik_matches_oracle_on_the_same_model(w2v):
+# d = 100, 300 and 600 take the kernels with 2, 5 and 10 elements per lane; window 5 and 10 put up to 10
+# and 20 words in a centre's window, more than one group of words for the d = 300 kernel (8 per walk)
+@pytest.mark.parametrize("dim,window,n_held", [(100, 5, None), (300, 5, 200_000), (300, 10, 200_000),
+                                                (600, 5, 200_000)])
+def test_loglik_matches_oracle_on_the_same_model(w2v, dim, window, n_held):
+    log(f"loglik d={dim} window={window}")
     s = oracle_side("sg_v30k_d100")
     voc, tree = gpu_side(w2v, s)
-    syn0, syn1 = synth.init_weights(s.voc.V, s.w.dim, syn1_scale=0.3)
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=30.0 / math.sqrt(dim))
+    syn0 = syn0 * np.float32(dim / 5)   # entries up to 0.1: dot products of order 1 at every d
     model = w2v.make_model(syn0, syn1, voc, tree)
-    held = corpus("sg_v30k_d100", heldout=True)
+    held = corpus("sg_v30k_d100", heldout=True)[:n_held]
     hv = oracle.remap(held, s.voc.id_to_vocab)
-    p = w2v.Params(window=5, sample=1e-3, seed=synth.SEED_EVAL)
+    p = w2v.Params(window=window, sample=1e-3, seed=synth.SEED_EVAL)
     sg, npg, nng = w2v.hs_loglik(model, to_dev(hv), p)
-    op = oracle.params(s.voc.V, s.w.dim, window=5, sample=1e-3, train_words=s.voc.train_words, seed=synth.SEED_EVAL)
+    op = oracle.params(s.voc.V, dim, window=window, sample=1e-3, train_words=s.voc.train_words,
+                       seed=synth.SEED_EVAL)
     so, npo, nno = oracle.loglik(syn0, syn1, s.tree, hv, op)
     assert (npg, nng) == (npo, nno)
     assert abs(sg - so) <= 1e-6 * abs(so)
