@@ -2,8 +2,11 @@
 GPU (through the C ABI): empty and fully dropped streams, documents too short
 for a window, the smallest tree (V = 2) and vector size (d = 1), a ragged last
 document, a corpus fed in whole-document chunks, the widest window, rows
-packed with no padding, and padding columns that hold NaN.
+packed with no padding, padding columns that hold NaN, and the deepest tree
+the codes allow (64 levels).
 """
+import types
+
 import numpy as np
 import pytest
 
@@ -272,3 +275,47 @@ def test_delta_only_cache_lds_budget(w2v):
     with pytest.raises(w2v.W2VError) as e:
         w2v.train_hs_epoch(model, to_dev(s.tv[:2000]), p)
     assert e.value.code == w2v.W2V_E_ARG and "LDS" in str(e.value)
+
+
+# The deepest tree the 64-bit codes allow: Fibonacci counts over 65 words give paths of 1 to 64 inner
+# nodes (one leaf at each depth up to 63, two at 64), so a path fills all 64 lanes of a wavefront and its
+# last code bit is bit 63. Training on a stream that visits every word, and the log-likelihood of the
+# trained model, match the oracle; the cache covers the top 31 of the 64 levels or none of them.
+@pytest.mark.parametrize("dim,k,wp,arch", [(300, 31, 15, 0), (300, 31, 5, 0), (100, 7, 1, 0), (64, 0, 0, 0),
+                                          (300, 31, 15, 1), (100, 31, 5, 2)])
+def test_deepest_tree_matches_oracle(w2v, dim, k, wp, arch):
+    fib = [1, 1]
+    while len(fib) < 65:
+        fib.append(fib[-1] + fib[-2])
+    counts = np.array(sorted(fib, reverse=True), np.int64)
+    V = counts.size
+    ot = oracle.build_huffman(counts)
+    assert int(ot.codelen.max()) == 64
+    tree = w2v.build_huffman(to_dev(counts))
+    assert tree.max_len == 64
+    np.testing.assert_array_equal(tree.code.cpu().numpy().view(np.uint64), ot.code)
+    np.testing.assert_array_equal(tree.points.cpu().numpy(), ot.points)
+    voc = types.SimpleNamespace(vocab_counts=to_dev(counts), train_words=int(counts.sum()))
+    tv = np.random.default_rng(11).integers(0, V, 3000).astype(np.int32)
+    syn0, syn1 = synth.init_weights(V, dim, syn1_scale=0.5 / dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(V, dim, window=5, sample=0.0, train_words=voc.train_words, corpus_tokens=tv.size,
+                       cache_k=k, flush_every=10, order=0 if arch == 2 else 1, orient=1 if arch == 2 else 0,
+                       arch=1 if arch == 1 else 0)
+    ost = oracle.train(a0, a1, ot, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=0.0, corpus_tokens=tv.size, cache_k=k, flush_every=10, workers=1,
+                   write_policy=wp, arch=arch)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:V - 1], a1) <= 1e-4
+    # the held-out objective of the oracle's trained model, walked over the full 64-node paths
+    pe = oracle.params(V, dim, window=5, sample=0.0, train_words=voc.train_words, seed=synth.SEED_EVAL,
+                       arch=1 if arch == 1 else 0)
+    so, npo, nno = oracle.loglik(a0, a1, ot, tv, pe)
+    sg, npg, nng = w2v.hs_loglik(w2v.make_model(a0, a1, voc, tree), to_dev(tv),
+                                 w2v.Params(window=5, sample=0.0, seed=synth.SEED_EVAL, arch=1 if arch == 1 else 0))
+    assert (npg, nng) == (npo, nno)
+    assert abs(sg - so) <= 1e-6 * abs(so)
+
