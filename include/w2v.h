@@ -210,8 +210,11 @@ typedef struct {
  * the paper's Hogwild setting, except with workers=1.
  * mode 1: every gradient of a batch of sync_batch consecutive kept centres
  * uses the model at the start of the batch; the sums (exact int64 fixed
- * point) are applied at its end. Deterministic. Synchronises the stream once
- * (to read the number of kept centres).
+ * point, 40 fraction bits) are applied at its end. Deterministic. A row's
+ * change within one batch must stay below 2^23 in magnitude (the fixed
+ * point's range); a batch that large has diverged (e.g. batches of hundreds
+ * of centres over a vocabulary of a few dozen words). Synchronises the
+ * stream once (to read the number of kept centres).
  * stats: int64[W2V_N_STATS] device buffer, overwritten (may be NULL).
  * Errors: W2V_E_ARG for a bad model/params (V < 2, dim not in 1..1024,
  * window not in 1..10, cache_mode not 0 or 1, LDS budget exceeded: 2 cache_k

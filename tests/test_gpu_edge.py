@@ -277,6 +277,13 @@ def test_delta_only_cache_lds_budget(w2v):
     assert e.value.code == w2v.W2V_E_ARG and "LDS" in str(e.value)
 
 
+def fib_counts():
+    fib = [1, 1]
+    while len(fib) < 65:
+        fib.append(fib[-1] + fib[-2])
+    return np.array(sorted(fib, reverse=True), np.int64)
+
+
 # The deepest tree the 64-bit codes allow: Fibonacci counts over 65 words give paths of 1 to 64 inner
 # nodes (one leaf at each depth up to 63, two at 64), so a path fills all 64 lanes of a wavefront and its
 # last code bit is bit 63. Training on a stream that visits every word, and the log-likelihood of the
@@ -284,10 +291,7 @@ def test_delta_only_cache_lds_budget(w2v):
 @pytest.mark.parametrize("dim,k,wp,arch", [(300, 31, 15, 0), (300, 31, 5, 0), (100, 7, 1, 0), (64, 0, 0, 0),
                                           (300, 31, 15, 1), (100, 31, 5, 2)])
 def test_deepest_tree_matches_oracle(w2v, dim, k, wp, arch):
-    fib = [1, 1]
-    while len(fib) < 65:
-        fib.append(fib[-1] + fib[-2])
-    counts = np.array(sorted(fib, reverse=True), np.int64)
+    counts = fib_counts()
     V = counts.size
     ot = oracle.build_huffman(counts)
     assert int(ot.codelen.max()) == 64
@@ -318,4 +322,29 @@ def test_deepest_tree_matches_oracle(w2v, dim, k, wp, arch):
                                  w2v.Params(window=5, sample=0.0, seed=synth.SEED_EVAL, arch=1 if arch == 1 else 0))
     assert (npg, nng) == (npo, nno)
     assert abs(sg - so) <= 1e-6 * abs(so)
+
+
+# Synchronous mode on the deepest tree: batches of 32 centres against a snapshot, 64-node paths. (With
+# batches of 256 over these 65 words every row takes dozens of summed changes per batch and the model
+# diverges on both sides -- the oracle reaches 1e14 -- past the range of the GPU's fixed-point sums.)
+@pytest.mark.parametrize("dim", [100, 300])
+def test_deepest_tree_sync_mode_matches_oracle(w2v, dim):
+    counts = fib_counts()
+    V = counts.size
+    ot = oracle.build_huffman(counts)
+    tree = w2v.build_huffman(to_dev(counts))
+    voc = types.SimpleNamespace(vocab_counts=to_dev(counts), train_words=int(counts.sum()))
+    tv = np.random.default_rng(12).integers(0, V, 3000).astype(np.int32)
+    syn0, syn1 = synth.init_weights(V, dim, syn1_scale=0.5 / dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(V, dim, window=5, sample=0.0, train_words=voc.train_words, corpus_tokens=tv.size,
+                       sync_batch=32)
+    ost = oracle.train_sync(a0, a1, ot, tv, op, n_batches=-1)
+    assert np.abs(a0).max() < 10 and np.abs(a1).max() < 10   # a regime that does not diverge
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=0.0, corpus_tokens=tv.size, mode=1, sync_batch=32)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:V - 1], a1) <= 1e-4
 
