@@ -121,6 +121,30 @@ def test_ragged_last_document(w2v, n):
     assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
 
 
+# The longest documents (65,535 raw tokens: 16-bit offsets, up to 512 segments of kept centres) at raw
+# positions past 2^32, with the learning rate of a later epoch: one worker against the oracle.
+@pytest.mark.parametrize("dim,wp,arch", [(100, 5, 0), (300, 15, 0), (300, 15, 1)])
+def test_longest_documents_far_into_the_run(w2v, dim, wp, arch):
+    s = oracle_side("sg_v30k_d100")
+    voc = w2v.build_vocab(to_dev(s.tok), s.w.vocab, s.w.min_count)
+    tree = w2v.build_huffman(voc.vocab_counts)
+    tv = s.tv[:70_000]   # one whole document (about 50,000 kept centres, 390 segments) and a ragged one
+    first, doc_len, corpus = 65535 * 70_000, 65535, 5_000_000_000
+    syn0, syn1 = synth.init_weights(s.voc.V, dim, syn1_scale=0.5 / dim)
+    a0, a1 = syn0.copy(), syn1.copy()
+    op = oracle.params(s.voc.V, dim, window=5, sample=1e-3, train_words=s.voc.train_words, corpus_tokens=corpus,
+                       doc_len=doc_len, first_raw_index=first, epoch=1, n_epochs=3, order=1, cache_k=31,
+                       flush_every=10, arch=arch)
+    ost = oracle.train(a0, a1, s.tree, tv, op)
+    model = w2v.make_model(syn0, syn1, voc, tree)
+    p = w2v.Params(window=5, sample=1e-3, corpus_tokens=corpus, doc_len=doc_len, first_raw_index=first, epoch=1,
+                   n_epochs=3, workers=1, cache_k=31, flush_every=10, write_policy=wp, arch=arch)
+    st = w2v.train_hs_epoch(model, to_dev(tv), p).cpu().numpy()
+    assert list(st) == list(ost)
+    g0, g1 = (t.cpu().numpy() for t in model.vectors())
+    assert row_rel_err(g0, a0) <= 1e-4 and row_rel_err(g1[:s.voc.V - 1], a1) <= 1e-4
+
+
 @pytest.mark.parametrize("arch", [0, 2])
 def test_chunked_stream_equals_whole_stream(w2v, arch):
     # without a cache one worker's result depends only on the centre sequence and the raw positions,

@@ -176,6 +176,9 @@ def pairs_both(w2v, s, tv, **kw):
     ("tiny_sg_v1k_d50", None, dict(window=10, doc_len=333)),
     ("sg_v30k_d100", 2_000_500, {}),                     # ragged last document
     ("sg_v30k_d100", 2_000_000, dict(first=7_000_000, epoch=2, seed=11)),
+    # raw positions past 2^32 (the counter's high word) and the longest documents the 16-bit offsets hold
+    ("sg_v30k_d100", 1_000_000, dict(first=6_000_000_000, epoch=1, seed=5)),
+    ("sg_v30k_d100", 400_000, dict(doc_len=65535, first=65535 * 70_000)),
 ])
 def test_pairs_bit_exact(w2v, name, n, kw):
     s = oracle_side(name)
