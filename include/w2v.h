@@ -284,9 +284,9 @@ int w2v_hs_loglik(const w2v_model *m, const int32_t *tokens, int64_t n_tokens, c
  * library runs on holds until the process ends. The call itself allocates
  * nothing; its first call on a device looks up that device's copy of the
  * array. Evaluations whose w2v_hs_loglik_workspace_bytes exceed the scratch
- * return W2V_E_RANGE before anything is launched (8 bytes per token plus
- * 8 bytes per vocabulary word and some per-document counts: e.g. V = 1M
- * with up to about 6M tokens). Every call on a device shares that device's
+ * return W2V_E_RANGE before anything is launched (about 11 bytes per token
+ * with 1,000-token documents, plus 8 bytes per vocabulary word: e.g. V = 1M
+ * with up to about 5.3M tokens). Every call on a device shares that device's
  * scratch, which keeps the last call's contents: calls that overlap on one
  * device (other streams or threads) race on it and must not be issued
  * concurrently. Synchronises the stream.
