@@ -37,7 +37,7 @@ size_t ns_train_extra_bytes();
 int launch_train_ns(const w2v_model *m, const int32_t *table, int32_t log2_size, const w2v_params *p,
                     const SampleBufs &b, int64_t n_tokens, const float *alpha_tab, int64_t blk0, Carve &c,
                     hipEvent_t ev0, hipEvent_t ev1, int64_t *stats, hipStream_t s);
-size_t ns_objective_extra_bytes(int64_t n_docs);
+size_t ns_objective_extra_bytes(int64_t n_docs, int32_t doc_len);
 int run_ns_objective(const w2v_model *m, const int32_t *table, int32_t log2_size, const w2v_params *p,
                      const SampleBufs &b, int64_t n_tokens, Carve &c, double *sum_host, int64_t *n_pairs_host,
                      int64_t *n_terms_host, hipStream_t s);
@@ -504,7 +504,7 @@ size_t w2v_ns_objective_workspace_bytes(const w2v_model *m, int64_t n_tokens, co
     if (!m || !p || p->doc_len < 1 || m->V < 2) return 0;
     Carve c;
     sample_bufs_carve(c, m->V, n_tokens, p->doc_len);
-    return c.used() + ns_objective_extra_bytes(std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len)));
+    return c.used() + ns_objective_extra_bytes(std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len)), p->doc_len);
 }
 
 int w2v_ns_objective(const w2v_model *m, const int32_t *noise_table, int32_t log2_size, const int32_t *tokens,

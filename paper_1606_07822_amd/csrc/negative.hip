@@ -158,6 +158,11 @@ __device__ __forceinline__ double log_sigmoid(double u) {
     return fmin(u, 0.0) - log1p(exp(-fabs(u)));
 }
 
+// Held-out objective work units: kObjSeg kept centres (short units keep the read-only walk's latency spread
+// over many wavefronts, as in the hierarchical-softmax evaluation).
+constexpr int kObjSeg = 8;
+inline int32_t obj_segs_per_doc(int32_t doc_len) { return static_cast<int32_t>(ceil_div(doc_len, kObjSeg)); }
+
 // ------------------------------------------------------------ training
 struct NsArgs {
     float *syn0;
@@ -182,8 +187,10 @@ struct NsArgs {
     int32_t write_policy;    // bit 0: target rows stored, bit 1: word rows stored (else atomic adds)
     int32_t *queue;
     unsigned long long *stats;   // [3]: kept, pairs, pair-target updates
-    // objective
-    double *doc_sum;
+    // objective: units of kObjSeg consecutive kept centres of one document, one wavefront each
+    int32_t obj_segs_per_doc;
+    int64_t obj_units;
+    double *doc_sum;     // per objective unit
     int64_t *doc_terms;
 };
 
@@ -350,12 +357,15 @@ __global__ __launch_bounds__(256) void k_ns_objective(NsArgs a) {
     const int lane = lane_id();
     const int64_t wave0 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
     const int64_t nwaves = static_cast<int64_t>(gridDim.x) * blockDim.x / kWave;
-    for (int64_t d = wave0; d < a.n_docs; d += nwaves) {
+    for (int64_t u = wave0; u < a.obj_units; u += nwaves) {
+        const int64_t d = u / a.obj_segs_per_doc;
         const int nk = a.doc_kept[d];
+        const int j0 = static_cast<int>(u - d * a.obj_segs_per_doc) * kObjSeg;
+        const int j1 = min(nk, j0 + kObjSeg);
         const int64_t base = d * a.doc_len;
         double acc = 0.0;
         int64_t terms = 0;
-        for (int j = 0; j < nk; ++j) {
+        for (int j = j0; j < j1; ++j) {
             const uint32_t meta = a.kept_meta[base + j];
             const int v = a.kept_vid[base + j];
             const int eff = static_cast<int>(meta >> 16);
@@ -396,8 +406,8 @@ __global__ __launch_bounds__(256) void k_ns_objective(NsArgs a) {
         }
         acc = wave_sum(acc);
         if (lane == 0) {
-            a.doc_sum[d] = acc;
-            a.doc_terms[d] = terms;
+            a.doc_sum[u] = acc;
+            a.doc_terms[u] = terms;
         }
     }
 }
@@ -620,10 +630,11 @@ int launch_train_ns(const w2v_model *m, const int32_t *table, int32_t log2_size,
     return W2V_OK;
 }
 
-size_t ns_objective_extra_bytes(int64_t n_docs) {
+size_t ns_objective_extra_bytes(int64_t n_docs, int32_t doc_len) {
+    const int64_t units = n_docs * obj_segs_per_doc(doc_len);
     Carve c;
-    c.take<double>(static_cast<size_t>(n_docs));
-    c.take<int64_t>(static_cast<size_t>(n_docs));
+    c.take<double>(static_cast<size_t>(units));
+    c.take<int64_t>(static_cast<size_t>(units));
     c.take<double>(1);
     c.take<int64_t>(1);
     return c.used();
@@ -634,18 +645,21 @@ int run_ns_objective(const w2v_model *m, const int32_t *table, int32_t log2_size
                      int64_t *n_terms_host, hipStream_t s) {
     NsArgs a = ns_args(m, table, log2_size, p, b, n_tokens);
     const int64_t n_docs = std::max<int64_t>(1, ceil_div(n_tokens, p->doc_len));
-    a.doc_sum = c.take<double>(static_cast<size_t>(n_docs));
-    a.doc_terms = c.take<int64_t>(static_cast<size_t>(n_docs));
+    a.obj_segs_per_doc = obj_segs_per_doc(p->doc_len);
+    a.obj_units = a.n_docs * a.obj_segs_per_doc;
+    const int64_t units_cap = n_docs * a.obj_segs_per_doc;
+    a.doc_sum = c.take<double>(static_cast<size_t>(units_cap));
+    a.doc_terms = c.take<int64_t>(static_cast<size_t>(units_cap));
     double *out = c.take<double>(1);
     int64_t *out_t = c.take<int64_t>(1);
     if (a.n_docs > 0) {
-        const unsigned grid =
-            static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_docs, 4), 16LL * device_cu_count()));
+        // one unit per wavefront: the hardware hands out workgroups as others finish
+        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(ceil_div(a.obj_units, 4), INT32_MAX));
         NsFn fn = pick_ns(m->dim, p->negative, true);
         if (!fn) return fail(W2V_E_ARG, "no kernel variant for this dim and number of negatives");
         hipLaunchKernelGGL(fn, dim3(grid), dim3(256), 0, s, a);
         W2V_LAUNCH_CHECK("k_ns_objective");
-        k_sum_docs_ns<<<1, 1024, 0, s>>>(a.doc_sum, a.doc_terms, a.n_docs, out, out_t);
+        k_sum_docs_ns<<<1, 1024, 0, s>>>(a.doc_sum, a.doc_terms, a.obj_units, out, out_t);
         W2V_LAUNCH_CHECK("k_sum_docs_ns");
     }
     double hs = 0.0;
