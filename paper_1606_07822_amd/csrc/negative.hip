@@ -58,33 +58,11 @@ __global__ void k_noise_weights(const int64_t *__restrict__ counts, int32_t V, i
     }
 }
 
-// exclusive scan of n int64 (one block); out[n] = total
-__global__ __launch_bounds__(1024) void k_scan_weights(const int64_t *__restrict__ in, int64_t n,
-                                                       int64_t *__restrict__ out) {
-    __shared__ int64_t wsum[16];
-    __shared__ int64_t carry;
-    if (threadIdx.x == 0) carry = 0;
-    __syncthreads();
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    for (int64_t base = 0; base < n; base += 1024) {
-        const int64_t i = base + threadIdx.x;
-        const int64_t x = i < n ? in[i] : 0;
-        int64_t inc = x;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int64_t y = __shfl_up(inc, d, 64);
-            if (lane >= d) inc += y;
-        }
-        if (lane == 63) wsum[wid] = inc;
-        __syncthreads();
-        int64_t before = carry;
-        for (int w = 0; w < wid; ++w) before += wsum[w];
-        if (i < n) out[i] = before + inc - x;
-        __syncthreads();
-        if (threadIdx.x == 1023) carry = before + inc;
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) out[n] = carry;
+// exclusive scan of n int64 (one workgroup); out[n] = total
+__global__ __launch_bounds__(kScanThreads) void k_scan_weights(const int64_t *__restrict__ in, int64_t n,
+                                                               int64_t *__restrict__ out) {
+    const int64_t total = block_exclusive_scan(in, n, out);
+    if (threadIdx.x == 0) out[n] = total;
 }
 
 // word v fills entries [ceil(Q[v] T / Q), ceil(Q[v+1] T / Q)): exactly the i with
@@ -439,32 +417,10 @@ __global__ __launch_bounds__(1024) void k_sum_docs_ns(const double *__restrict__
     }
 }
 
-// exclusive scan of per-document kept counts (int32) into int64 offsets (one block)
-__global__ __launch_bounds__(1024) void k_scan_kept_ns(const int32_t *__restrict__ in, int64_t n,
-                                                       int64_t *__restrict__ out) {
-    __shared__ int64_t wsum[16];
-    __shared__ int64_t carry;
-    if (threadIdx.x == 0) carry = 0;
-    __syncthreads();
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    for (int64_t b = 0; b < n; b += 1024) {
-        const int64_t i = b + threadIdx.x;
-        const int64_t x = i < n ? in[i] : 0;
-        int64_t inc = x;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int64_t yv = __shfl_up(inc, d, 64);
-            if (lane >= d) inc += yv;
-        }
-        if (lane == 63) wsum[wid] = inc;
-        __syncthreads();
-        int64_t before = carry;
-        for (int w = 0; w < wid; ++w) before += wsum[w];
-        if (i < n) out[i] = before + inc - x;
-        __syncthreads();
-        if (threadIdx.x == 1023) carry = before + inc;
-        __syncthreads();
-    }
+// exclusive scan of per-document kept counts (int32) into int64 offsets (one workgroup)
+__global__ __launch_bounds__(kScanThreads) void k_scan_kept_ns(const int32_t *__restrict__ in, int64_t n,
+                                                               int64_t *__restrict__ out) {
+    block_exclusive_scan(in, n, out);
 }
 
 // Test hook: every kept centre's negatives (stream order) and their checksum.
@@ -576,7 +532,7 @@ int run_noise_table(const int64_t *vocab_counts, int32_t V, int32_t log2_size, i
     const unsigned g = static_cast<unsigned>(std::min<int64_t>(ceil_div(V, 256), 4096));
     k_noise_weights<<<g, 256, 0, s>>>(vocab_counts, V, w);
     W2V_LAUNCH_CHECK("k_noise_weights");
-    k_scan_weights<<<1, 1024, 0, s>>>(w, V, pre);
+    k_scan_weights<<<1, kScanThreads, 0, s>>>(w, V, pre);
     W2V_LAUNCH_CHECK("k_scan_weights");
     int64_t tot = 0;
     W2V_HIP(hipMemcpyAsync(&tot, pre + V, sizeof(tot), hipMemcpyDeviceToHost, s));
@@ -695,7 +651,7 @@ int run_ns_negatives(const w2v_params *p, const int32_t *table, int32_t log2_siz
     k_zero_ns<<<1, 64, 0, s>>>(nullptr, cs);
     W2V_LAUNCH_CHECK("k_zero_ns");
     if (a.n_docs > 0) {
-        k_scan_kept_ns<<<1, 1024, 0, s>>>(b.doc_kept, a.n_docs, doc_off);
+        k_scan_kept_ns<<<1, kScanThreads, 0, s>>>(b.doc_kept, a.n_docs, doc_off);
         W2V_LAUNCH_CHECK("k_scan_kept_ns");
         const unsigned grid =
             static_cast<unsigned>(std::min<int64_t>(ceil_div(a.n_docs, 4), 16LL * device_cu_count()));

@@ -179,32 +179,10 @@ int launch_alpha_table(const w2v_params *p, int64_t blk0, int64_t nblk, float *t
 // ------------------------------------------------------------ pair listing
 namespace {
 
-// exclusive scan of doc_pairs (int64) over n_docs, one block
-__global__ __launch_bounds__(1024) void k_scan_i64(const int64_t *__restrict__ in, int64_t n,
-                                                   int64_t *__restrict__ out) {
-    __shared__ int64_t wsum[16];
-    __shared__ int64_t carry;
-    if (threadIdx.x == 0) carry = 0;
-    __syncthreads();
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    for (int64_t base = 0; base < n; base += 1024) {
-        const int64_t i = base + threadIdx.x;
-        const int64_t x = i < n ? in[i] : 0;
-        int64_t inc = x;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int64_t y = __shfl_up(inc, d, 64);
-            if (lane >= d) inc += y;
-        }
-        if (lane == 63) wsum[wid] = inc;
-        __syncthreads();
-        int64_t before = carry;
-        for (int w = 0; w < wid; ++w) before += wsum[w];
-        if (i < n) out[i] = before + inc - x;
-        __syncthreads();
-        if (threadIdx.x == 1023) carry = before + inc;
-        __syncthreads();
-    }
+// exclusive scan of doc_pairs (int64) over n_docs (one workgroup)
+__global__ __launch_bounds__(kScanThreads) void k_scan_i64(const int64_t *__restrict__ in, int64_t n,
+                                                           int64_t *__restrict__ out) {
+    block_exclusive_scan(in, n, out);
 }
 
 // one wave per document: write its pairs at the document's offset; checksum of all pairs
@@ -289,7 +267,7 @@ int run_sample_pairs(const int32_t *tokens, int64_t n_tokens, int32_t V, const i
     k_zero_u64s<<<1, 64, 0, s>>>(cs, 2);
     W2V_LAUNCH_CHECK("k_zero_u64s");
     if (n_tokens > 0) {
-        k_scan_i64<<<1, 1024, 0, s>>>(b.doc_pairs, ceil_div(n_tokens, p->doc_len), doc_off);
+        k_scan_i64<<<1, kScanThreads, 0, s>>>(b.doc_pairs, ceil_div(n_tokens, p->doc_len), doc_off);
         W2V_LAUNCH_CHECK("k_scan_i64");
         const unsigned grid = static_cast<unsigned>(
             std::min<int64_t>(ceil_div(ceil_div(n_tokens, p->doc_len), 4), 16LL * device_cu_count()));

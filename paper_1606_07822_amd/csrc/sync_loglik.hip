@@ -160,31 +160,10 @@ __global__ void k_zero_i32_range(int32_t *p, int64_t n) {
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0;
 }
 
-__global__ __launch_bounds__(1024) void k_scan_kept(const int32_t *__restrict__ in, int64_t n,
-                                                    int64_t *__restrict__ out) {
-    __shared__ int64_t wsum[16];
-    __shared__ int64_t carry;
-    if (threadIdx.x == 0) carry = 0;
-    __syncthreads();
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    for (int64_t base = 0; base < n; base += 1024) {
-        const int64_t i = base + threadIdx.x;
-        const int64_t x = i < n ? in[i] : 0;
-        int64_t inc = x;
-#pragma unroll
-        for (int dd = 1; dd < 64; dd <<= 1) {
-            const int64_t y = __shfl_up(inc, dd, 64);
-            if (lane >= dd) inc += y;
-        }
-        if (lane == 63) wsum[wid] = inc;
-        __syncthreads();
-        int64_t before = carry;
-        for (int w = 0; w < wid; ++w) before += wsum[w];
-        if (i < n) out[i] = before + inc - x;
-        __syncthreads();
-        if (threadIdx.x == 1023) carry = before + inc;
-        __syncthreads();
-    }
+// exclusive scan of per-document kept counts (int32) into int64 offsets
+__global__ __launch_bounds__(kScanThreads) void k_scan_kept(const int32_t *__restrict__ in, int64_t n,
+                                                            int64_t *__restrict__ out) {
+    block_exclusive_scan(in, n, out);
 }
 
 using SyncFn = void (*)(SyncArgs);
@@ -249,7 +228,7 @@ int run_train_sync(const w2v_model *m, const w2v_params *p, const SampleBufs &b,
     k_zero_i32_range<<<static_cast<unsigned>(ceil_div(2LL * m->V, 256)), 256, 0, s>>>(fl, 2LL * m->V);
     k_reset_counts<<<1, 64, 0, s>>>(a.cnt);
     if (n_tokens <= 0) return W2V_OK;
-    k_scan_kept<<<1, 1024, 0, s>>>(b.doc_kept, a.n_docs, kept_off);
+    k_scan_kept<<<1, kScanThreads, 0, s>>>(b.doc_kept, a.n_docs, kept_off);
     W2V_LAUNCH_CHECK("sync setup");
     int64_t tot[4];
     W2V_HIP(hipMemcpyAsync(tot, b.totals, sizeof(tot), hipMemcpyDeviceToHost, s));
