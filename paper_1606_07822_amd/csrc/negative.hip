@@ -34,6 +34,7 @@
 #include <algorithm>
 
 #include "w2v_internal.h"
+#include "w2v_scan.h"
 
 namespace w2v {
 namespace {

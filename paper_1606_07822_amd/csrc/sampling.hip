@@ -12,6 +12,7 @@
 #include <algorithm>
 
 #include "w2v_internal.h"
+#include "w2v_scan.h"
 
 namespace w2v {
 namespace {
