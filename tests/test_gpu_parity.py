@@ -427,6 +427,8 @@ def test_single_worker_cbow_span_with_hot_rows(w2v, name, sample, k, dim):
     (0, "tiny_sg_v1k_d50", 0.0, 31, 300, 0), (0, "sg_v30k_d100", 1e-3, 31, 300, 0), (0, "sg_v30k_d100", 1e-3, 0, 200, 0),
     (1, "tiny_sg_v1k_d50", 0.0, 31, 300, 0), (0, "tiny_sg_v1k_d50", 0.0, 54, 300, 0),
     (0, "tiny_sg_v1k_d50", 0.0, 31, 300, 40), (0, "sg_v30k_d100", 1e-3, 31, 300, 2000),
+    # the benchmark's LDS: 48 cached rows and their originals beside the centre records and the stash
+    (0, "sg_v30k_d100", 1e-3, 48, 300, 2000), (1, "sg_v30k_d100", 1e-3, 48, 300, 0),
 ])
 def test_single_worker_span_stash_matches_oracle(w2v, arch, name, sample, k, dim, sfrom):
     log(f"span stash arch={arch} {name} t={sample} k={k} dim={dim} from={sfrom}")

@@ -39,10 +39,10 @@ def test_full_epoch_in_bench_launch(w2v):
     held = to_dev(oracle.remap(corpus(NAME, heldout=True), ov.id_to_vocab))
     pe = w2v.Params(window=w.window, sample=w.sample, seed=synth.SEED_EVAL)
     ref = golden(f"oracle_ll_{NAME}.json")
-    # bench.py's settings: every row stored, word rows kept across centres (write_policy 15), the old
-    # centre's row back from the stash for words of index >= 10000
+    # bench.py's settings: the top 31 inner nodes cached, every row stored, word rows kept across centres
+    # (write_policy 15), the old centre's row back from the stash for words of index >= 10000
     p = w2v.Params(window=w.window, sample=w.sample, alpha0=w.alpha0, corpus_tokens=w.n_tokens,
-                   seed=synth.SEED_TRAIN, write_policy=15, span_stash=1, stash_from=10000)
+                   seed=synth.SEED_TRAIN, cache_k=31, write_policy=15, span_stash=1, stash_from=10000)
 
     def run():
         model = w2v.make_model(syn0, syn1, voc, tree)
