@@ -86,8 +86,9 @@ int w2v_build_vocab(const int32_t *tokens, int64_t n_tokens, int32_t id_space, i
  *   points     int32[points_cap] out; NULL = size query (only codelen, code,
  *                           point_off and the host outputs are written)
  *   points_len_host, max_len_host  out: sum of code lengths, longest code
- * Errors: W2V_E_ARG if V < 2 or points_cap < sum of lengths (points given);
- * W2V_E_RANGE if a code would be longer than 64. Synchronises the stream.
+ * Errors: W2V_E_ARG if V < 2, vocab_counts is not in descending order, or
+ * points_cap < sum of lengths (points given); W2V_E_RANGE if a code would be
+ * longer than 64. Synchronises the stream.
  * ---------------------------------------------------------------------- */
 size_t w2v_build_huffman_workspace_bytes(int32_t V);
 int w2v_build_huffman(const int64_t *vocab_counts, int32_t V, uint8_t *codelen, uint64_t *code,
