@@ -122,7 +122,8 @@ typedef struct {
                                 2 = skip-gram with the reversed orientation: for each window word w in order
                                 the path of w is walked with the centre's vector as input, which gains that
                                 pair's hidden-layer gradient before the next pair (asynchronous mode only) */
-    int32_t mode;            /* 0 = asynchronous (lock-free, top-k cache in LDS), 1 = synchronous batches */
+    int32_t mode;            /* 0 = asynchronous (lock-free, top-k cache in LDS), 1 = synchronous batches
+                                (skip-gram, arch 0, only) */
     int32_t window;          /* W ("windowsize", §4.1), 1..10; effective half-width uniform on 1..W */
     int32_t doc_len;         /* documents of doc_len raw tokens (1..65535); windows never cross them */
     double sample;           /* subsampling threshold t ("downsample", §4.1); 0 = keep all */
