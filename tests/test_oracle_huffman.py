@@ -8,7 +8,10 @@ What fixes these other than the oracle itself:
     sequence, found by exhaustive search (V <= 8);
   * the construction rule (two-queue merge, leaf wins ties, first child gets
     bit 0) by an independent quadratic "scan for the minimum" construction;
-  * textbook special cases (V = 2; 2^m equal counts give length m).
+  * textbook special cases (V = 2; 2^m equal counts give length m);
+  * the generation-wise construction that the GPU's parallel merge follows
+    (each generation's picks are a stable merge of the leaf queue with the
+    inner nodes it started with) gives the same tree, bit for bit.
 """
 import functools
 import math
@@ -189,3 +192,78 @@ def test_code_longer_than_64_bits_is_rejected():
 def test_v_below_two_is_rejected():
     with pytest.raises(ValueError):
         oracle.build_huffman(np.array([5], np.int64))
+
+
+# ---------------------------------------------------------------- generations
+def generation_tree(counts):
+    """The tree built generation by generation: while an inner node that existed when a generation began is
+    still queued, the inner front is such an "old" node, so the generation's picks are the stable merge of
+    the leaf queue with the old nodes (a leaf first on a tie), cut after the last old node; merge a0 + j
+    takes picks 2j (bit 0) and 2j + 1 (bit 1). An odd last pick (the last old node) opens one more merge
+    with the smaller of the leaf front and the generation's first node. (The GPU builds the tree so.)"""
+    V = counts.size
+    leaf = counts[::-1].astype(np.int64)                      # ascending; position p is word V-1-p
+    icount = np.zeros(max(V - 1, 1), np.int64)
+    parent = np.full(2 * V - 1, -1, np.int32)
+    bit = np.zeros(2 * V - 1, np.uint8)
+    pl = ih = a = 0
+
+    def put(child, node, b):
+        parent[child] = node
+        bit[child] = b
+
+    while a < V - 1:
+        a0 = a
+        if a0 == ih:                                          # no inner node yet: two leaves
+            put(V - 1 - pl, a, 0)
+            put(V - 2 - pl, a, 1)
+            icount[a] = leaf[pl] + leaf[pl + 1]
+            pl, a = pl + 2, a + 1
+            continue
+        old = icount[ih:a0]
+        nl = int(np.searchsorted(leaf[pl:], old[-1], side="right"))   # leaves at most the last old count
+        vals = np.concatenate([leaf[pl:pl + nl], old])
+        ids = np.concatenate([V - 1 - (pl + np.arange(nl)), V + ih + np.arange(old.size)])
+        # stable merge, leaves before old nodes on a tie (leaves come first in the concatenation)
+        order = np.argsort(vals, kind="stable")
+        vals, ids = vals[order], ids[order]
+        m = vals.size // 2
+        for j in range(m):
+            put(ids[2 * j], a0 + j, 0)
+            put(ids[2 * j + 1], a0 + j, 1)
+        icount[a0:a0 + m] = vals[0:2 * m:2] + vals[1:2 * m:2]
+        a = a0 + m
+        pl, ih = pl + nl, a0
+        if vals.size % 2:                                     # the last old node opens one more merge
+            put(ids[-1], a, 0)
+            if pl < V and (a == a0 or leaf[pl] <= icount[a0]):
+                put(V - 1 - pl, a, 1)
+                icount[a] = vals[-1] + leaf[pl]
+                pl += 1
+            else:
+                put(V + a0, a, 1)
+                icount[a] = vals[-1] + icount[a0]
+                ih += 1
+            a += 1
+    return parent, bit
+
+
+@pytest.mark.parametrize("V,hi,seed", [(2, 9, 1), (3, 2, 2), (5, 3, 3), (64, 2, 4), (1000, 5, 5), (1000, 10**6, 6),
+                                       (30_000, 50, 7)])
+def test_generation_wise_construction_equals_the_two_queue_merge(V, hi, seed):
+    rng = np.random.default_rng(seed)
+    counts = np.sort(rng.integers(1, hi, V))[::-1].astype(np.int64)
+    t = oracle.build_huffman(counts)
+    parent, bit = generation_tree(counts)
+    np.testing.assert_array_equal(parent, t.parent)
+    np.testing.assert_array_equal(bit, t.bit)
+
+
+def test_generation_wise_construction_on_zipf_and_equal_counts():
+    p = 1.0 / np.arange(1, 20_001) ** 1.05
+    for counts in (np.maximum(np.floor(p / p.sum() * 1e8), 5).astype(np.int64), np.full(4096, 7, np.int64)):
+        counts = np.sort(counts)[::-1].copy()
+        t = oracle.build_huffman(counts)
+        parent, bit = generation_tree(counts)
+        np.testing.assert_array_equal(parent, t.parent)
+        np.testing.assert_array_equal(bit, t.bit)
