@@ -28,8 +28,9 @@ namespace {
 //
 // One block computes a generation in chunks of kChunk elements of S: it copies the next
 // kChunk leaves and old counts to LDS, and thread j finds how many leaves precede
-// element 2j by a binary search on the merge path (the largest i with A[i-1] <= B[2j-i]
-// and B[2j-i-1] < A[i], A the leaves, B the old nodes), then takes its two picks.
+// element 2j by a binary search on the merge path (the i with A[i-1] <= B[2j-i] and
+// B[2j-i-1] < A[i], A the leaves, B the old nodes, a missing neighbour passing its
+// test), then takes its two picks.
 constexpr int kMergeThreads = 1024;
 constexpr int kChunk = 2 * kMergeThreads;   // elements of S per chunk: one merge per thread
 
