@@ -140,6 +140,25 @@ def test_huffman_few_distinct_counts_bit_exact(w2v, V, seed):
     check_tree(w2v, np.sort(rng.choice([1, 2, 3, 5, 8, 1000], V))[::-1].astype(np.int64))
 
 
+# Sizes around the parallel merge's chunk (2,048 picks) and count shapes that give long and short
+# generations: uniform, few distinct values, geometric-like, heavy-tailed.
+@pytest.mark.parametrize("case", range(24))
+def test_huffman_varied_shapes_bit_exact(w2v, case):
+    rng = np.random.default_rng(100 + case)
+    V = [2, 3, 4, 1023, 1024, 1025, 2047, 2048, 2049, 4095, 4097, 6145][case % 12] if case < 12 else \
+        int(rng.integers(2, 60_000))
+    kind = case % 4
+    if kind == 0:
+        counts = rng.integers(1, 1000, V)
+    elif kind == 1:
+        counts = rng.choice([1, 1, 2, 3, 100], V)
+    elif kind == 2:
+        counts = np.floor(1.5 ** rng.uniform(0, 40, V)).astype(np.int64) + 1
+    else:
+        counts = np.floor(1e6 / rng.pareto(1.1, V).clip(1e-3)).astype(np.int64) + 1
+    check_tree(w2v, np.sort(counts.astype(np.int64))[::-1].copy())
+
+
 def test_huffman_too_deep_is_an_error(w2v):
     fib = [1, 1]
     while len(fib) < 70:
