@@ -63,11 +63,23 @@ def test_vocab_bit_exact(w2v, name, n):
     np.testing.assert_array_equal(voc.tokens.cpu().numpy(), s.tv)
 
 
-@pytest.mark.parametrize("case", ["empty", "single_id", "min_count_0", "id_space_1", "ragged_big_space", "all_dropped"])
+@pytest.mark.parametrize("case", ["empty", "single_id", "min_count_0", "id_space_1", "ragged_big_space", "all_dropped",
+                                  "lds_bin_edge", "unaligned_stream"])
 def test_vocab_edge_cases(w2v, case):
     rng = np.random.default_rng(5)
     id_space, mc = 1000, 5
-    if case == "empty":
+    offset = 0
+    if case == "lds_bin_edge":
+        # ids on both sides of the count kernel's LDS bins (36,864) and at the end of the id space
+        id_space = 36_866
+        tok = np.concatenate([rng.integers(36_860, 36_866, 50_000), rng.integers(0, 8, 50_000),
+                              rng.integers(0, id_space, 1_001)]).astype(np.int32)
+        rng.shuffle(tok)
+    elif case == "unaligned_stream":
+        # a stream that starts 4 bytes past a 16-byte boundary: the remap takes its one-token path
+        tok = rng.integers(0, 300, 100_003).astype(np.int32)
+        offset = 1
+    elif case == "empty":
         tok = np.zeros(0, np.int32)
     elif case == "single_id":
         tok = np.full(777, 3, np.int32)
@@ -80,12 +92,17 @@ def test_vocab_edge_cases(w2v, case):
         tok = (rng.zipf(1.1, 2_000_003) % id_space).astype(np.int32)
     else:
         tok = np.arange(1000, dtype=np.int32)
-    voc = w2v.build_vocab(to_dev(tok) if tok.size else to_dev(np.zeros(1, np.int32))[:0], id_space, mc)
+    if offset:
+        dev = to_dev(np.concatenate([np.zeros(offset, np.int32), tok]))[offset:]
+    else:
+        dev = to_dev(tok) if tok.size else to_dev(np.zeros(1, np.int32))[:0]
+    voc = w2v.build_vocab(dev, id_space, mc)
     o = oracle.build_vocab(tok, id_space, mc)
     assert voc.V == o.V and voc.train_words == o.train_words
     np.testing.assert_array_equal(voc.counts_by_id.cpu().numpy(), o.counts)
     np.testing.assert_array_equal(voc.vocab_ids.cpu().numpy(), o.vocab_ids)
     np.testing.assert_array_equal(voc.id_to_vocab.cpu().numpy(), o.id_to_vocab)
+    np.testing.assert_array_equal(voc.tokens.cpu().numpy(), oracle.remap(tok, o.id_to_vocab))
 
 
 def test_vocab_out_of_range_token_is_an_error(w2v):
